@@ -1,0 +1,279 @@
+#!/usr/bin/env python3
+"""Aggregate decode throughput of the owner-scoped fast-weight READ/WRITE path.
+
+Workload: 8 request streams at 4B-class shape (d_model 2560, d_ff 9728), 36
+fast-weight layers, bf16 activations, fp32 fast-weight state; each stream does
+64 READ decode steps then one C=64 WRITE, phases staggered by 8 steps so most
+steps mix READ owners and a WRITE owner.  One benchmark step is one decode
+step of all 8 streams through every layer: rwttt_plan, the READ group's
+launches, the WRITE group's token launches and update launches, and the
+commits -- the whole hot path.  Every WRITE step also emits its token, so a
+step yields 8 tokens.
+
+Inputs are seeded synthetic tensors, resident in HBM before timing starts.
+The timed region is bracketed by torch.cuda.synchronize().  Each launch is
+also bracketed by HIP events on the launch stream; the READ kernel's average
+bandwidth over the timed region gives the roofline fraction.  The CPU oracle
+is then timed on a bounded sample of the same trace.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "aggregate decode tok/s (8 TTT streams, 1 GPU); % HBM peak READ, % MFMA WRITE"
+HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class LaunchTimer:
+    """HIP events around every launch, on torch's current stream."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.records = []
+        self._open = None
+
+    def begin(self, kind, count, chunk):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record()
+        self._open = (kind, count, chunk, e)
+
+    def end(self):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record()
+        kind, count, chunk, s = self._open
+        self.records.append((kind, count, chunk, s, e))
+
+    def summary(self, wl):
+        K, N = wl.d_ff, wl.d_model
+        io, st = wl.io_bytes, (4 if wl.state_dtype == "f32" else 2)
+        out = {}
+        for kind in ("read", "write"):
+            recs = [r for r in self.records if r[0] == kind]
+            if not recs:
+                continue
+            ms = sum(s.elapsed_time(e) for _, _, _, s, e in recs)
+            if kind == "read":
+                byt = sum(K * N * (io + b * st) + b * io * (K + N) for _, b, _, _, _ in recs)
+                flop = sum(4.0 * b * K * N for _, b, _, _, _ in recs)
+            else:
+                byt = sum(b * (2 * st * K * N + io * c * (K + N)) for _, b, c, _, _ in recs)
+                flop = sum(2.0 * b * c * K * N for _, b, c, _, _ in recs)
+            out[kind] = dict(launches=len(recs), total_ms=ms, avg_us=1e3 * ms / len(recs),
+                             bytes=byt, flops=flop,
+                             gbs=byt / (ms * 1e-3) / 1e9, tflops=flop / (ms * 1e-3) / 1e12)
+        return out
+
+
+def prepare(wl, layers, n_steps, threads, keep_layers):
+    """Device-resident state and inputs for steps [0, n_steps)."""
+    import torch
+    from rwttt_inputs import TensorSource, WRITE
+    from rwttt_inputs.schedule import step_items
+    from paper_2605_28053_amd.serving import Session, to_device
+
+    src = TensorSource(wl, cache_steps=False)
+    sess = Session(wl, None, layers, init_state=False, init_w0=False)
+    kept = {}
+    with ThreadPoolExecutor(threads) as ex:
+        for i, arr in enumerate(ex.map(src.w0, layers)):
+            to_device(arr, wl.io_dtype, out=sess.w0[i])
+        jobs = [(r, i, l) for r in range(wl.n_owners) for i, l in enumerate(layers)]
+        for lo in range(0, len(jobs), 2 * threads):
+            part = jobs[lo:lo + 2 * threads]
+            for (r, i, l), arr in zip(part, ex.map(lambda j: src.dw_init(j[0], j[2]), part)):
+                to_device(arr, wl.state_dtype, out=sess.slots[r][i][0])
+                if l in keep_layers:
+                    kept[(r, l)] = arr
+        log(f"state resident: {len(jobs)} slots of {wl.state_bytes / 1e6:.1f} MB")
+
+        L, Rn = len(layers), wl.n_owners
+        X = torch.empty((n_steps, L, Rn, wl.d_ff), dtype=torch.bfloat16, device="cuda")
+        lidx = np.array(layers)
+
+        def xs(t):
+            return np.ascontiguousarray(src.x_step(t)[:, lidx].transpose(1, 0, 2))
+
+        for t, arr in enumerate(ex.map(xs, range(n_steps))):
+            to_device(arr, wl.io_dtype, out=X[t])
+        writes = [(t, it.owner, it.chunk) for t in range(n_steps)
+                  for it in step_items(wl, t) if it.effect == WRITE]
+
+        def zg(w):
+            Z, G = src.zg_owner(*w)
+            return Z[lidx], G[lidx]
+
+        ZG = {}
+        for (t, r, c), (Z, G) in zip(writes, ex.map(zg, writes)):
+            zd, gd = to_device(Z, wl.io_dtype), to_device(G, wl.io_dtype)
+            ZG[(t, r)] = (zd, gd, [zd[i].data_ptr() for i in range(L)],
+                          [gd[i].data_ptr() for i in range(L)])
+    Y = torch.empty((L, Rn, wl.d_model), dtype=torch.bfloat16, device="cuda")
+    torch.cuda.synchronize()
+    return sess, X, Y, ZG, kept
+
+
+def run_gpu(args, wl, layers):
+    import torch
+    from rwttt_inputs.schedule import step_items
+
+    n = args.warmup + args.steps
+    t0 = time.time()
+    keep = set(args.cpu_layers) if args.cpu_baseline == "on" else set()
+    sess, X, Y, ZG, kept = prepare(wl, layers, n, args.threads, keep)
+    log(f"setup {time.time() - t0:.1f} s")
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    y_ptrs = [Y[i].data_ptr() for i in range(len(layers))]
+
+    def one(t, timer=None):
+        items = step_items(wl, t)
+        x_ptrs = [X[t, i].data_ptr() for i in range(len(layers))]
+        zg = {r: (ZG[(t, r)][2], ZG[(t, r)][3]) for r in [it.owner for it in items] if (t, r) in ZG}
+        res = sess.step(t, items, x_ptrs, y_ptrs, zg, sp, timer=timer)
+        return sum(1 for it in items if it.emit), res
+
+    for t in range(args.warmup):
+        one(t)
+    torch.cuda.synchronize()
+    timer = LaunchTimer(torch) if args.kernel_events == "on" else None
+    tokens = 0
+    writes = 0
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for t in range(args.warmup, n):
+        k, res = one(t, timer)
+        tokens += k
+        writes += len(res.committed) + len(res.rolled_back)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    kern = timer.summary(wl) if timer is not None else {}
+    versions = sess.versions()
+    sess.close()
+    return dict(tokens=tokens, elapsed=elapsed, kernels=kern, versions=versions,
+                writes=writes, kept=kept)
+
+
+def run_cpu_baseline(args, wl, kept):
+    """The oracle as it stands, on steps [0, S) of the same trace, a layer subset."""
+    import oracle as O
+    from rwttt_inputs import TensorSource, build_trace
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()
+                            if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        blas_threads = os.cpu_count()
+    layers = list(args.cpu_layers)
+    steps = range(args.cpu_steps)
+    trace = build_trace(wl, args.cpu_steps)
+    src = TensorSource(wl)
+    table = O.OwnerTable(wl.n_owners, layers)
+    for r in range(wl.n_owners):
+        for l in layers:
+            arr = kept.get((r, l))
+            table.D[(r, l)] = O.widen(arr if arr is not None else src.dw_init(r, l), wl.state_dtype)
+    for t in steps:                       # draw the inputs outside the timed window
+        src.x_step(t)
+    t0 = time.perf_counter()
+    records, _ = O.run_trace(wl, trace, src, steps=steps, layers=layers, table=table)
+    dt = time.perf_counter() - t0
+    tokens = sum(len(rec.y) for rec in records) / len(layers)
+    scale = wl.n_layers / len(layers)
+    return dict(value=tokens / (dt * scale), unit="tok/s", cores=int(blas_threads), kind="oracle",
+                sample=(f"float64 numpy oracle on decode steps 0-{args.cpu_steps - 1} of the same "
+                        f"trace, layers {layers} of {wl.n_layers}, all {wl.n_owners} owners; "
+                        f"{dt:.2f} s measured, scaled x{scale:g} to all layers"))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=260)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--layers", type=int, default=None, help="fast-weight layers (default 36)")
+    ap.add_argument("--threads", type=int, default=16, help="host threads for input generation")
+    ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
+    ap.add_argument("--cpu-steps", type=int, default=30)
+    ap.add_argument("--cpu-layers", type=int, nargs="+", default=[0, 1])
+    ap.add_argument("--kernel-events", choices=["on", "off"], default="on")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(owners would shard across GPUs with no exchange); run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    from rwttt_inputs import workload
+    wl = workload(2)
+    layers = list(range(wl.n_layers if args.layers is None else args.layers))
+
+    g = run_gpu(args, wl, layers)
+    tok_s = g["tokens"] / g["elapsed"]
+    kern = g["kernels"]
+    line = {
+        "metric": METRIC,
+        "value": round(tok_s, 2),
+        "unit": "tok/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(1e3 * g["elapsed"] / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: 8 streams, {len(layers)} fast-weight layers, d_model "
+                        f"{wl.d_model}, d_ff {wl.d_ff}, bf16 io, fp32 state, 64 READ steps then "
+                        f"one C=64 WRITE per stream, phases staggered by 8",
+            "owners": wl.n_owners, "layers": len(layers), "d_model": wl.d_model, "d_ff": wl.d_ff,
+            "io": wl.io_dtype, "state": wl.state_dtype, "accumulate": "f32",
+            "write_chunk": wl.chunk, "tokens_timed": g["tokens"], "writes_timed": g["writes"],
+            "parallelism": "single-gpu",
+        },
+    }
+    if "read" in kern:
+        rd = kern["read"]
+        line["roofline"] = {"bound": "hbm", "kernel": "read_kernel",
+                            "achieved": round(rd["gbs"], 1), "peak": HBM_PEAK_GBS,
+                            "unit": "GB/s", "frac": round(rd["gbs"] / HBM_PEAK_GBS, 4),
+                            "traffic": None, "avg_launch_us": round(rd["avg_us"], 2),
+                            "launches": rd["launches"]}
+    if "write" in kern:
+        wr = kern["write"]
+        line["write_kernel"] = {"achieved_gbs": round(wr["gbs"], 1),
+                                "hbm_frac": round(wr["gbs"] / HBM_PEAK_GBS, 4),
+                                "achieved_tflops": round(wr["tflops"], 2),
+                                "mfma_frac": round(wr["tflops"] / BF16_MFMA_PEAK_TFLOPS, 5),
+                                "avg_launch_us": round(wr["avg_us"], 2), "launches": wr["launches"]}
+    if args.cpu_baseline == "on":
+        line["cpu_baseline"] = run_cpu_baseline(args, wl, g["kept"])
+    line["paper_context"] = ("274.61 tok/s, 9.31x over sequential serving: full Qwen3-4B "
+                             "In-Place-TTT model, 8 streams, one unnamed GPU (not this metric)")
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

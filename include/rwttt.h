@@ -1,0 +1,218 @@
+/*
+ * rwttt.h -- C ABI of the owner-scoped fast-weight READ/WRITE path of
+ * read-write TTT serving (RW-TTT, Yang et al.), for AMD Instinct MI355X
+ * (gfx950).
+ *
+ * Every request r owns a versioned fast-weight delta dW_r per layer, added to
+ * the shared down-projection W0 (Section 3, request tuple and Ownership;
+ * Section 4.1, FastWeightState).  The library keeps, per (owner, layer), two
+ * caller-allocated device slots: the live slot holds the committed version
+ * V(r), the other is the shadow that receives a WRITE's dirty candidate.
+ * Commit flips which slot is live; rollback forgets the shadow.  Neither
+ * copies state.
+ *
+ * Conventions for every entry point:
+ *  - Returns an rwttt_status: RWTTT_OK (0) or a negative error code.
+ *  - Arguments are validated before anything changes; on error the owner
+ *    table is left as it was and nothing is launched.
+ *  - Device pointers are plain HIP device addresses, 16-byte aligned.  The
+ *    caller allocates and frees all device memory (weights, slots, inputs,
+ *    outputs, workspace); the library never allocates or frees device memory
+ *    and never synchronises the stream it is given.
+ *  - Host arrays are read during the call only; the library keeps no pointer
+ *    to them, except the config's pointer tables, which it copies.
+ *  - Matrices are row-major.  Shapes: W0 and every slot [d_ff, d_model];
+ *    x [n_owners, d_ff]; y [n_owners, d_model]; Z [C, d_ff]; G [C, d_model].
+ *  - A context is not thread-safe; use one per host thread.
+ */
+#ifndef RWTTT_H
+#define RWTTT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t rwttt_status;
+
+/* status codes */
+#define RWTTT_OK               0
+#define RWTTT_DEFERRED         1   /* per-event plan status: held back by the wait budget */
+#define RWTTT_E_INVALID       -1   /* bad argument, shape, pointer or owner id          */
+#define RWTTT_E_STALE_VERSION -2   /* event's expected version differs from V(r)        */
+#define RWTTT_E_OWNER_ALIAS   -3   /* one owner appears twice in an event set or group  */
+#define RWTTT_E_KEY_MISMATCH  -4   /* wrong effect for the call                         */
+#define RWTTT_E_NOT_DIRTY     -5   /* commit/rollback of an owner with no candidate     */
+#define RWTTT_E_DIRTY         -6   /* owner already holds an uncommitted candidate      */
+#define RWTTT_E_CAPACITY      -7   /* an output array is too small                      */
+#define RWTTT_E_HIP           -8   /* HIP launch or runtime error; see rwttt_last_hip_error */
+#define RWTTT_E_WRITE_FAILED  -9   /* a WRITE of this owner failed; it can only roll back */
+
+/* state effect rho (Section 3, eq. event) */
+#define RWTTT_READ  0
+#define RWTTT_WRITE 1
+
+/* element types */
+#define RWTTT_F32  0
+#define RWTTT_BF16 1   /* bfloat16, round-to-nearest-even on every narrowing */
+
+/* largest owner group one rwttt_read / rwttt_write call accepts */
+#define RWTTT_MAX_GROUP 64
+
+typedef struct rwttt_ctx rwttt_ctx;
+
+/* One ready transition e_i = (r_i, tau_i, sigma_i, rho_i, v_i) plus its ready
+ * step (Section 3, eqs. event and wait-budget).  The planner compares
+ * backend_type, shape_class and placement only for equality and order. */
+typedef struct rwttt_event {
+    uint32_t owner;             /* r: owner id, < n_owners                     */
+    uint32_t backend_type;      /* tau: backend state type                     */
+    uint32_t shape_class;       /* sigma: operator shape class (opaque)        */
+    uint32_t placement;         /* pi: placement (device)                      */
+    int32_t  effect;            /* rho: RWTTT_READ or RWTTT_WRITE              */
+    uint32_t reserved;          /* must be 0                                   */
+    uint64_t expected_version;  /* v_i, checked against V(r_i)                 */
+    uint64_t ready_step;        /* decode step at which the event became ready */
+} rwttt_event;
+
+/* One legal group: all members share kappa = (rho, tau, sigma, pi); its
+ * owner map is owner_map[first .. first+count) (Section 4.3). */
+typedef struct rwttt_group {
+    int32_t  effect;
+    uint32_t backend_type;
+    uint32_t shape_class;
+    uint32_t placement;
+    uint32_t first;
+    uint32_t count;
+} rwttt_group;
+
+typedef struct rwttt_config {
+    uint32_t n_owners;          /* number of request owners                       */
+    uint32_t n_layers;          /* fast-weight layers per owner                   */
+    uint32_t d_ff;              /* rows of W0 and of each slot; multiple of 8     */
+    uint32_t d_model;           /* columns; multiple of 8                         */
+    int32_t  io_dtype;          /* RWTTT_F32 / RWTTT_BF16: x, W0, y, Z, G         */
+    int32_t  state_dtype;       /* RWTTT_F32 / RWTTT_BF16: fast-weight slots      */
+    uint32_t max_group;         /* largest READ group, 1..RWTTT_MAX_GROUP         */
+    uint32_t reserved;          /* must be 0                                      */
+    const void* const* w0;      /* [n_layers] device pointers to W0_l             */
+    void* const* slots;         /* [n_owners*n_layers*2] device pointers; entry
+                                   (owner*n_layers + layer)*2 + s is slot s.
+                                   Slot 0 holds version 0 and starts live.       */
+    void* workspace;            /* device buffer of rwttt_workspace_bytes() bytes,
+                                   or NULL for a host-only context (planning and
+                                   the owner table; rwttt_read/_write then fail) */
+    size_t workspace_bytes;
+} rwttt_config;
+
+/* Bytes of device workspace a context with this config needs: the READ
+ * split-K partial sums, max_group x ceil(d_ff/256) x d_model fp32 values
+ * (d_model rounded up to the column tile).  Only the shape fields and
+ * max_group are read.  The workspace needs no initialisation. */
+rwttt_status rwttt_workspace_bytes(const rwttt_config* cfg, size_t* bytes);
+
+/* Create a context: copies the pointer tables, sets V(r) = 0, slot 0 live and
+ * no candidate for every owner.  Makes no HIP call.  Slot pointers must be
+ * pairwise distinct (RWTTT_E_OWNER_ALIAS otherwise).  *out is set only on
+ * success; release with rwttt_destroy. */
+rwttt_status rwttt_create(const rwttt_config* cfg, rwttt_ctx** out);
+rwttt_status rwttt_destroy(rwttt_ctx* ctx);
+
+/* LegalGroups (Algorithm 1; Section 3 eqs. compatibility and wait-budget;
+ * Section 4.3).  Host-only, integer-only, reads the owner table and changes
+ * nothing.
+ *   ev[n_ev]        ready events at decode step `step`.
+ *   target_b        target group size B (0: no size target).
+ *   wait_budget     w: a partial group is issued only when w == 0 or its
+ *                   oldest member has waited w steps; otherwise deferred.
+ * Outputs: groups[0 .. *n_groups) in key order (effect, backend_type,
+ * shape_class, placement as unsigned integers, READ first), each group's
+ * members in (ready_step, owner) order, concatenated in owner_map; deferred
+ * event indices in the same order; ev_status[i] = RWTTT_OK (issued),
+ * RWTTT_DEFERRED, or a rejection: RWTTT_E_INVALID (bad owner/effect, or
+ * ready_step > step), RWTTT_E_DIRTY (owner holds a candidate),
+ * RWTTT_E_STALE_VERSION (expected_version != V(owner)).
+ * Returns RWTTT_E_OWNER_ALIAS if two events name one owner (then no output is
+ * meaningful), RWTTT_E_CAPACITY if groups_cap, map_cap or deferred_cap is too
+ * small (*n_groups, *n_mapped and *n_deferred then hold the sizes needed). */
+rwttt_status rwttt_plan(const rwttt_ctx* ctx, const rwttt_event* ev, uint32_t n_ev,
+                        uint64_t step, uint32_t target_b, uint32_t wait_budget,
+                        rwttt_group* groups, uint32_t groups_cap, uint32_t* n_groups,
+                        uint32_t* owner_map, uint32_t map_cap, uint32_t* n_mapped,
+                        uint32_t* deferred, uint32_t deferred_cap, uint32_t* n_deferred,
+                        int32_t* ev_status);
+
+/* READ / ApplyState (Section 3, Read; Section 4.2 primitives table): for each
+ * slot b of the group, owner r = owner_map[first+b]:
+ *     y[r, :] = x[r, :] W0_layer + x[r, :] dW_{r,layer}^live
+ * accumulated in fp32 and rounded once to the io dtype.  Versions and slots
+ * are unchanged.  Also emits the token of a WRITE step, read at version v
+ * before its candidate is committed (Section 3, Write returns y; Section 4.1,
+ * the candidate is invisible until commit), so `group` may have either
+ * effect.  x and y are owner-indexed: only the group's rows are read or
+ * written, which returns outputs through the owner map (Algorithm 1,
+ * ReturnOutputs).  y must not overlap x, W0 or any slot.  Results for an owner
+ * are bit-identical whatever the group's size, order or other members.
+ * An empty group returns RWTTT_OK and launches nothing.  Launches two kernels
+ * on `stream` (split-K partial sums into the workspace, then their reduction);
+ * the workspace is shared by all reads of a context, so reads of one context
+ * must be ordered on the device (one stream, or event waits). */
+rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
+                        uint32_t layer, const void* x, void* y, void* stream);
+
+/* WRITE / BoundaryUpdate (Section 3, Write; Section 4.2 "WRITE"): for each
+ * slot b, owner r = owner_map[first+b]:
+ *     shadow_{r,layer} = live_{r,layer} + eta * Z_b^T G_b
+ * with Z_b = z[b] ([chunk, d_ff]) and G_b = g[b] ([chunk, d_model]); the
+ * product accumulates in fp32 and the result is rounded once to the state
+ * dtype.  `z` and `g` are host arrays of group.count device pointers.  The
+ * group must have effect RWTTT_WRITE.  Marks each owner dirty (its write view
+ * is open until commit or rollback, Section 4.1).  Errors: RWTTT_E_DIRTY if
+ * this layer of an owner was already written in the open transition.  If the
+ * launch fails (RWTTT_E_HIP) or a failure was injected (RWTTT_E_WRITE_FAILED),
+ * the owners stay dirty and are marked failed: they can only roll back. */
+rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
+                         uint32_t layer, uint32_t chunk, const void* const* z,
+                         const void* const* g, float eta, void* stream);
+
+/* Commit (Section 4.2 CONTROL; Algorithm 1, CommitVersions): for each owner,
+ * flip the live slot of every layer written in its open transition and set
+ * V(r) = V(r) + 1.  Host-only, O(owners), copies nothing.  All owners are
+ * validated first: RWTTT_E_NOT_DIRTY (no candidate), RWTTT_E_WRITE_FAILED
+ * (its WRITE failed), RWTTT_E_OWNER_ALIAS (listed twice).  Later launches see
+ * the new live slot; they must be ordered after the WRITE on the device (same
+ * stream, or an event wait). */
+rwttt_status rwttt_commit(rwttt_ctx* ctx, const uint32_t* owners, uint32_t n);
+
+/* Rollback (Section 4.2 CONTROL; the failure branch of Algorithm 1): forget
+ * each owner's candidate.  The live slots and V(r) are untouched, so version
+ * v is restored exactly.  Errors as for commit, except that failed owners are
+ * accepted. */
+rwttt_status rwttt_rollback(rwttt_ctx* ctx, const uint32_t* owners, uint32_t n);
+
+/* View (Algorithm 1): committed version, and whether a candidate is open. */
+rwttt_status rwttt_version(const rwttt_ctx* ctx, uint32_t owner, uint64_t* version, int32_t* dirty);
+
+/* Device address of the live (which = 0) or shadow (which = 1) slot of
+ * (owner, layer) as the table stands now. */
+rwttt_status rwttt_slot(const rwttt_ctx* ctx, uint32_t owner, uint32_t layer, int32_t which,
+                        void** ptr);
+
+/* Failure injection for state-contract tests (Section 5.5): the next `count`
+ * rwttt_write calls validate, mark their owners dirty and failed, launch
+ * nothing and return RWTTT_E_WRITE_FAILED. */
+rwttt_status rwttt_inject_write_failures(rwttt_ctx* ctx, uint32_t count);
+
+/* hipError_t of the last RWTTT_E_HIP returned by this context (0 if none). */
+int32_t rwttt_last_hip_error(const rwttt_ctx* ctx);
+
+/* Static description of a status code. */
+const char* rwttt_strerror(rwttt_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RWTTT_H */

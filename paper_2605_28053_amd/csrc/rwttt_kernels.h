@@ -1,0 +1,56 @@
+// Internal launch interface between the host library (rwttt_api.cpp) and the
+// gfx950 kernels (rwttt_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "rwttt.h"
+
+namespace rwttt {
+
+// READ tiling.  A work item is (group slot, K chunk, column tile).  The chunk
+// and tile sizes depend only on the matrix shape, never on the group, so an
+// owner's result does not depend on who else is in the group.
+constexpr int kReadThreads = 256;     // 4 wave64s
+constexpr int kReadChunk = 256;       // K rows per work item
+
+inline int read_cols_per_lane(int state_bf16) { return state_bf16 ? 8 : 4; }   // 16 B per lane
+inline int read_tile_n(int state_bf16) { return 64 * read_cols_per_lane(state_bf16); }
+
+struct ReadGeometry {
+  int ks;       // K chunks
+  int nt;       // column tiles
+  int npad;     // nt * tile_n
+  size_t part_floats;    // partial sums: max_group * ks * npad
+  size_t total_bytes;    // workspace bytes, 256-B aligned
+};
+
+ReadGeometry read_geometry(int d_ff, int d_model, int state_bf16, int max_group);
+
+struct ReadLaunch {
+  int io_bf16, state_bf16;
+  int d_ff, d_model, count, max_group;
+  const void* x;             // [n_owners, d_ff], owner-indexed
+  void* y;                   // [n_owners, d_model], owner-indexed
+  const void* w0;            // [d_ff, d_model]
+  void* workspace;           // ReadGeometry layout
+  const void* dw[RWTTT_MAX_GROUP];   // live slot of each group slot
+  uint32_t row[RWTTT_MAX_GROUP];     // owner id of each group slot
+};
+
+struct WriteLaunch {
+  int io_bf16, state_bf16;
+  int d_ff, d_model, count, chunk;
+  float eta;
+  const void* live[RWTTT_MAX_GROUP];
+  void* shadow[RWTTT_MAX_GROUP];
+  const void* z[RWTTT_MAX_GROUP];    // [chunk, d_ff]
+  const void* g[RWTTT_MAX_GROUP];    // [chunk, d_model]
+};
+
+hipError_t launch_read(const ReadLaunch& L, hipStream_t stream);
+hipError_t launch_write(const WriteLaunch& L, hipStream_t stream);
+
+}  // namespace rwttt

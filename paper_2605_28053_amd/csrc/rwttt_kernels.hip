@@ -1,0 +1,493 @@
+// gfx950 kernels of the owner-scoped fast-weight READ/WRITE path.
+//
+// READ  (ApplyState, Section 3 "Read"):   y_r = x_r W0 + x_r dW_r
+// WRITE (BoundaryUpdate, Section 3 "Write"): shadow_r = live_r + eta Z_r^T G_r
+//
+// Both operate on groups of owners, one launch per (group, layer).
+
+#include "rwttt_kernels.h"
+
+namespace rwttt {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+// ---------------------------------------------------------------------------
+// Number formats
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16 bits, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint32_t bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  __device__ static float get(const void* p, size_t i) { return static_cast<const float*>(p)[i]; }
+  __device__ static void put(void* p, size_t i, float v) { static_cast<float*>(p)[i] = v; }
+};
+template <> struct Elem<uint16_t> {
+  __device__ static float get(const void* p, size_t i) {
+    return __uint_as_float(uint32_t(static_cast<const uint16_t*>(p)[i]) << 16);
+  }
+  __device__ static void put(void* p, size_t i, float v) {
+    static_cast<uint16_t*>(p)[i] = static_cast<uint16_t>(bf16_rne(v));
+  }
+};
+
+// N consecutive elements at p as floats; p is 8-byte (N*2 == 8) or 16-byte aligned.
+template <int N> __device__ __forceinline__ void load_n(const float* p, float (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; i += 4) {
+    const float4 t = *reinterpret_cast<const float4*>(p + i);
+    v[i] = t.x; v[i + 1] = t.y; v[i + 2] = t.z; v[i + 3] = t.w;
+  }
+}
+template <int N> __device__ __forceinline__ void load_n(const uint16_t* p, float (&v)[N]) {
+  if constexpr (N == 8) {
+    const uint4 t = *reinterpret_cast<const uint4*>(p);
+    v[0] = bf16_lo(t.x); v[1] = bf16_hi(t.x); v[2] = bf16_lo(t.y); v[3] = bf16_hi(t.y);
+    v[4] = bf16_lo(t.z); v[5] = bf16_hi(t.z); v[6] = bf16_lo(t.w); v[7] = bf16_hi(t.w);
+  } else {
+    static_assert(N == 4, "bf16 loads are 4 or 8 wide");
+    const uint2 t = *reinterpret_cast<const uint2*>(p);
+    v[0] = bf16_lo(t.x); v[1] = bf16_hi(t.x); v[2] = bf16_lo(t.y); v[3] = bf16_hi(t.y);
+  }
+}
+
+template <int N> __device__ __forceinline__ void store_n(float* p, const float (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; i += 4)
+    *reinterpret_cast<float4*>(p + i) = make_float4(v[i], v[i + 1], v[i + 2], v[i + 3]);
+}
+template <int N> __device__ __forceinline__ void store_n(uint16_t* p, const float (&v)[N]) {
+  static_assert(N == 4, "bf16 stores are 4 wide");
+  uint2 t;
+  t.x = bf16_rne(v[0]) | (bf16_rne(v[1]) << 16);
+  t.y = bf16_rne(v[2]) | (bf16_rne(v[3]) << 16);
+  *reinterpret_cast<uint2*>(p) = t;
+}
+
+// ---------------------------------------------------------------------------
+// READ
+// ---------------------------------------------------------------------------
+//
+// y_b = x_b W0 + x_b dW_b, as two launches with no cross-block
+// synchronisation:
+//
+// 1. read_partial_kernel: one 256-thread block per (group slot b, K chunk of
+//    256 rows, column tile).  Each lane owns 16 contiguous bytes of every dW_b
+//    row of the tile (4 fp32 or 8 bf16 columns) and the same columns of W0;
+//    the four waves split the chunk's rows.  Per row it accumulates
+//    x[k]*dW[k] and then x[k]*W0[k] into one fp32 accumulator, so the shared
+//    W0 term is fused into the same pass.  The W0 tile is the same for every
+//    slot: the blocks of all slots for one (chunk, tile) are placed on one XCD
+//    (dispatch is round-robin over the 8 XCDs by block index) so that W0 comes
+//    from HBM once and is re-read from that XCD's L2.  dW is streamed with
+//    non-temporal loads so it does not evict W0.  The four waves' sums are
+//    added through LDS in a fixed order into one partial per (slot, chunk).
+// 2. read_reduce_kernel: y[b, n] = sum over chunks, in chunk order.
+//
+// Every order depends only on the matrix shape, so an owner's y is
+// bit-identical whatever the group's size, order or other members.
+
+struct ReadParams {
+  const void* x;
+  void* y;
+  const void* w0;
+  float* part;
+  int count, d_ff, d_model, ks, nt, npad;
+  const void* dw[RWTTT_MAX_GROUP];
+  uint32_t row[RWTTT_MAX_GROUP];
+};
+
+constexpr int kUnroll = 8;
+
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// N elements of T held packed in 32-bit words, converted to fp32 on use.
+template <typename T, int N> struct Packed {
+  static constexpr int W = N * int(sizeof(T)) / 4;
+  uint32_t w[W];
+  __device__ __forceinline__ float get(int i) const {
+    if constexpr (sizeof(T) == 4) return __uint_as_float(w[i]);
+    else return (i & 1) ? __uint_as_float(w[i >> 1] & 0xffff0000u) : __uint_as_float(w[i >> 1] << 16);
+  }
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int i = 0; i < W; ++i) w[i] = 0u;
+  }
+};
+
+template <bool NT, typename T, int N>
+__device__ __forceinline__ void load_packed(const T* p, Packed<T, N>& r) {
+  constexpr int W = Packed<T, N>::W;
+  static_assert(W == 2 || W % 4 == 0, "8- or 16-byte multiples");
+  if constexpr (W == 2) {
+    const u32x2_t t = NT ? __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p))
+                         : *reinterpret_cast<const u32x2_t*>(p);
+    r.w[0] = t[0];
+    r.w[1] = t[1];
+  } else {
+#pragma unroll
+    for (int i = 0; i < W; i += 4) {
+      const u32x4_t* q = reinterpret_cast<const u32x4_t*>(p) + i / 4;
+      const u32x4_t t = NT ? __builtin_nontemporal_load(q) : *q;
+      r.w[i] = t[0];
+      r.w[i + 1] = t[1];
+      r.w[i + 2] = t[2];
+      r.w[i + 3] = t[3];
+    }
+  }
+}
+
+template <typename IO, typename ST>
+__global__ void __launch_bounds__(kReadThreads) read_partial_kernel(const ReadParams p) {
+  constexpr int COLS = 16 / sizeof(ST);
+  constexpr int TILE_N = 64 * COLS;
+  constexpr int KC = kReadChunk;
+  constexpr int RW = KC / 4;
+  __shared__ float xs[KC];
+  __shared__ float red[4][TILE_N];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  // block -> (XCD, position on that XCD) -> ((chunk, tile) pair, slot)
+  const int xcd = blockIdx.x & 7;
+  const int pos = blockIdx.x >> 3;
+  const int pl = pos / p.count;
+  const int b = pos - pl * p.count;
+  const int pair = pl * 8 + xcd;
+  if (pair >= p.ks * p.nt) return;
+  const int kc = pair / p.nt;
+  const int nt = pair - kc * p.nt;
+  const int k0 = kc * KC;
+  const int kn = min(KC, p.d_ff - k0);
+  const int col = nt * TILE_N + lane * COLS;
+  const bool col_ok = col < p.d_model;
+
+  for (int k = tid; k < KC; k += kReadThreads)
+    xs[k] = k < kn ? Elem<IO>::get(p.x, size_t(p.row[b]) * p.d_ff + k0 + k) : 0.f;
+  __syncthreads();
+
+  const int kw0 = wave * RW;
+  const int kw1 = min(kw0 + RW, kn);
+  float acc[COLS];
+#pragma unroll
+  for (int c = 0; c < COLS; ++c) acc[c] = 0.f;
+  if (col_ok) {
+    const ST* dbase = static_cast<const ST*>(p.dw[b]) + size_t(k0) * p.d_model + col;
+    const IO* wbase = static_cast<const IO*>(p.w0) + size_t(k0) * p.d_model + col;
+    for (int k = kw0; k < kw1; k += kUnroll) {
+      Packed<ST, COLS> v[kUnroll];
+      Packed<IO, COLS> w[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        if (k + u < kw1) {
+          load_packed<true>(dbase + size_t(k + u) * p.d_model, v[u]);
+          load_packed<false>(wbase + size_t(k + u) * p.d_model, w[u]);
+        } else {
+          v[u].zero();
+          w[u].zero();
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const float xv = xs[k + u];
+#pragma unroll
+        for (int c = 0; c < COLS; ++c) acc[c] = fmaf(xv, w[u].get(c), fmaf(xv, v[u].get(c), acc[c]));
+      }
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < COLS; ++c) red[wave][lane * COLS + c] = acc[c];
+  __syncthreads();
+  float* dst = p.part + (size_t(b) * p.ks + kc) * p.npad + nt * TILE_N;
+  for (int j = tid; j < TILE_N; j += kReadThreads)
+    dst[j] = ((red[0][j] + red[1][j]) + red[2][j]) + red[3][j];
+}
+
+template <typename IO>
+__global__ void __launch_bounds__(256) read_reduce_kernel(const ReadParams p) {
+  const int b = blockIdx.y;
+  const int n = blockIdx.x * 256 + threadIdx.x;
+  if (n >= p.d_model) return;
+  const float* q = p.part + size_t(b) * p.ks * p.npad + n;
+  float s = 0.f;
+  int k = 0;
+  for (; k + 8 <= p.ks; k += 8) {
+    float a[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) a[u] = q[size_t(k + u) * p.npad];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += a[u];
+  }
+  for (; k < p.ks; ++k) s += q[size_t(k) * p.npad];
+  Elem<IO>::put(p.y, size_t(p.row[b]) * p.d_model + n, s);
+}
+
+// ---------------------------------------------------------------------------
+// WRITE, bf16 evidence: MFMA rank-C update
+// ---------------------------------------------------------------------------
+//
+// Block tile: 128 rows (d_ff, "m") x 64 columns (d_model, "n") of one owner's
+// slot.  The MFMA computes the transposed tile D[n][m] = sum_c G[c][n] Z[c][m]
+// (A = G^T, B = Z) so that each lane's four consecutive accumulator rows are
+// four consecutive columns of the row-major slot: the epilogue reads live and
+// writes shadow with one 16-byte access per four values, no LDS round trip.
+// Z and G chunks of 32 ranks are staged through LDS transposed to
+// rank-contiguous rows, which is the operand layout the MFMA reads (eight
+// consecutive ranks per lane).
+
+struct WriteParams {
+  int count, chunk, d_ff, d_model, mt, ntl;
+  float eta;
+  const void* live[RWTTT_MAX_GROUP];
+  void* shadow[RWTTT_MAX_GROUP];
+  const void* z[RWTTT_MAX_GROUP];
+  const void* g[RWTTT_MAX_GROUP];
+};
+
+constexpr int kWTM = 128;
+constexpr int kWTN = 64;
+constexpr int kWKC = 32;
+constexpr int kWPitch = kWKC + 8;   // bf16 elements per LDS row (80 B, 16-B aligned)
+
+template <typename ST>
+__global__ void __launch_bounds__(256) write_mfma_kernel(const WriteParams p) {
+  constexpr int SC = 4;   // state columns per accumulator group
+  __shared__ __attribute__((aligned(16))) uint16_t zt[kWTM * kWPitch];
+  __shared__ __attribute__((aligned(16))) uint16_t gt[kWTN * kWPitch];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int tiles = p.mt * p.ntl;
+  const int b = blockIdx.x / tiles;
+  const int rem = blockIdx.x - b * tiles;
+  const int mt = rem / p.ntl;
+  const int ntile = rem - mt * p.ntl;
+  const int m0 = mt * kWTM;
+  const int n0 = ntile * kWTN;
+  const ST* live = static_cast<const ST*>(p.live[b]);
+  ST* shadow = static_cast<ST*>(p.shadow[b]);
+  const uint16_t* Z = static_cast<const uint16_t*>(p.z[b]);
+  const uint16_t* G = static_cast<const uint16_t*>(p.g[b]);
+
+  const int half = lane >> 5;
+  const int m = m0 + wave * 32 + (lane & 31);
+  const bool m_ok = m < p.d_ff;
+
+  // Issue the live-state loads first; they are the bulk of the traffic.
+  float lv[2][4][SC];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int n = n0 + nb * 32 + q * 8 + half * 4;
+      if (m_ok && n < p.d_model) {
+        load_n<SC>(live + size_t(m) * p.d_model + n, lv[nb][q]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < SC; ++i) lv[nb][q][i] = 0.f;
+      }
+    }
+
+  f32x16_t acc0 = {}, acc1 = {};
+  for (int c0 = 0; c0 < p.chunk; c0 += kWKC) {
+    {  // Z chunk [32 ranks][128 m] -> zt[m][rank]
+      const int cp = tid >> 4;
+      const int mg = tid & 15;
+      const int mm = m0 + mg * 8;
+      const int c = c0 + 2 * cp;
+      uint4 r0 = make_uint4(0, 0, 0, 0), r1 = make_uint4(0, 0, 0, 0);
+      if (mm < p.d_ff) {
+        if (c < p.chunk) r0 = *reinterpret_cast<const uint4*>(Z + size_t(c) * p.d_ff + mm);
+        if (c + 1 < p.chunk) r1 = *reinterpret_cast<const uint4*>(Z + size_t(c + 1) * p.d_ff + mm);
+      }
+      const uint32_t a[4] = {r0.x, r0.y, r0.z, r0.w};
+      const uint32_t bb[4] = {r1.x, r1.y, r1.z, r1.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        *reinterpret_cast<uint32_t*>(&zt[(mg * 8 + 2 * j) * kWPitch + 2 * cp]) =
+            (a[j] & 0xffffu) | (bb[j] << 16);
+        *reinterpret_cast<uint32_t*>(&zt[(mg * 8 + 2 * j + 1) * kWPitch + 2 * cp]) =
+            (a[j] >> 16) | (bb[j] & 0xffff0000u);
+      }
+    }
+    if (tid < 128) {  // G chunk [32 ranks][64 n] -> gt[n][rank]
+      const int cp = tid >> 3;
+      const int ng = tid & 7;
+      const int nn = n0 + ng * 8;
+      const int c = c0 + 2 * cp;
+      uint4 r0 = make_uint4(0, 0, 0, 0), r1 = make_uint4(0, 0, 0, 0);
+      if (nn < p.d_model) {
+        if (c < p.chunk) r0 = *reinterpret_cast<const uint4*>(G + size_t(c) * p.d_model + nn);
+        if (c + 1 < p.chunk) r1 = *reinterpret_cast<const uint4*>(G + size_t(c + 1) * p.d_model + nn);
+      }
+      const uint32_t a[4] = {r0.x, r0.y, r0.z, r0.w};
+      const uint32_t bb[4] = {r1.x, r1.y, r1.z, r1.w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        *reinterpret_cast<uint32_t*>(&gt[(ng * 8 + 2 * j) * kWPitch + 2 * cp]) =
+            (a[j] & 0xffffu) | (bb[j] << 16);
+        *reinterpret_cast<uint32_t*>(&gt[(ng * 8 + 2 * j + 1) * kWPitch + 2 * cp]) =
+            (a[j] >> 16) | (bb[j] & 0xffff0000u);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < kWKC; ks += 16) {
+      const int kk = ks + half * 8;
+      const bf16x8_t bz = *reinterpret_cast<const bf16x8_t*>(&zt[(wave * 32 + (lane & 31)) * kWPitch + kk]);
+      const bf16x8_t a0 = *reinterpret_cast<const bf16x8_t*>(&gt[(lane & 31) * kWPitch + kk]);
+      const bf16x8_t a1 = *reinterpret_cast<const bf16x8_t*>(&gt[(32 + (lane & 31)) * kWPitch + kk]);
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, bz, acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, bz, acc1, 0, 0, 0);
+    }
+    __syncthreads();
+  }
+
+  // Accumulator register 4q+i of lane l holds D[8q + 4(l/32) + i][l % 32].
+  const float eta = p.eta;
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int n = n0 + nb * 32 + q * 8 + half * 4;
+      if (!(m_ok && n < p.d_model)) continue;
+      float out[SC];
+#pragma unroll
+      for (int i = 0; i < SC; ++i) {
+        const float a = nb == 0 ? acc0[4 * q + i] : acc1[4 * q + i];
+        out[i] = lv[nb][q][i] + eta * a;
+      }
+      store_n<SC>(shadow + size_t(m) * p.d_model + n, out);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// WRITE, fp32 evidence: VALU rank-C update (fp32 products keep the small
+// tiny-config tolerance; bf16 operands would round Z and G)
+// ---------------------------------------------------------------------------
+
+template <typename ST>
+__global__ void __launch_bounds__(256) write_valu_kernel(const WriteParams p) {
+  const int n4 = p.d_model / 4;
+  const size_t per_owner = size_t(p.d_ff) * n4;
+  const size_t gid = size_t(blockIdx.x) * 256 + threadIdx.x;
+  const int b = blockIdx.y;
+  if (gid >= per_owner) return;
+  const int m = int(gid / n4);
+  const int n = int(gid - size_t(m) * n4) * 4;
+  const float* Z = static_cast<const float*>(p.z[b]);
+  const float* G = static_cast<const float*>(p.g[b]);
+  float a[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < p.chunk; ++c) {
+    const float zc = Z[size_t(c) * p.d_ff + m];
+    const float4 g4 = *reinterpret_cast<const float4*>(G + size_t(c) * p.d_model + n);
+    a[0] = fmaf(zc, g4.x, a[0]);
+    a[1] = fmaf(zc, g4.y, a[1]);
+    a[2] = fmaf(zc, g4.z, a[2]);
+    a[3] = fmaf(zc, g4.w, a[3]);
+  }
+  const ST* live = static_cast<const ST*>(p.live[b]);
+  ST* shadow = static_cast<ST*>(p.shadow[b]);
+  float lv[4];
+  load_n<4>(live + size_t(m) * p.d_model + n, lv);
+  float out[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) out[i] = lv[i] + p.eta * a[i];
+  store_n<4>(shadow + size_t(m) * p.d_model + n, out);
+}
+
+template <typename IO, typename ST>
+hipError_t launch_read_t(const ReadLaunch& L, hipStream_t stream) {
+  const ReadGeometry g = read_geometry(L.d_ff, L.d_model, L.state_bf16, L.max_group);
+  ReadParams p;
+  p.x = L.x;
+  p.y = L.y;
+  p.w0 = L.w0;
+  p.part = static_cast<float*>(L.workspace);
+  p.count = L.count;
+  p.d_ff = L.d_ff;
+  p.d_model = L.d_model;
+  p.ks = g.ks;
+  p.nt = g.nt;
+  p.npad = g.npad;
+  for (int b = 0; b < RWTTT_MAX_GROUP; ++b) {
+    p.dw[b] = b < L.count ? L.dw[b] : nullptr;
+    p.row[b] = b < L.count ? L.row[b] : 0u;
+  }
+  // (chunk, tile) pairs rounded up to a multiple of the 8 XCDs
+  const unsigned pairs8 = unsigned((g.ks * g.nt + 7) / 8 * 8);
+  hipLaunchKernelGGL((read_partial_kernel<IO, ST>), dim3(pairs8 * unsigned(L.count)),
+                     dim3(kReadThreads), 0, stream, p);
+  hipLaunchKernelGGL((read_reduce_kernel<IO>), dim3((L.d_model + 255) / 256, L.count), dim3(256),
+                     0, stream, p);
+  return hipGetLastError();
+}
+
+template <typename ST>
+hipError_t launch_write_t(const WriteLaunch& L, hipStream_t stream) {
+  WriteParams p;
+  p.count = L.count;
+  p.chunk = L.chunk;
+  p.d_ff = L.d_ff;
+  p.d_model = L.d_model;
+  p.eta = L.eta;
+  p.mt = (L.d_ff + kWTM - 1) / kWTM;
+  p.ntl = (L.d_model + kWTN - 1) / kWTN;
+  for (int b = 0; b < RWTTT_MAX_GROUP; ++b) {
+    const bool in = b < L.count;
+    p.live[b] = in ? L.live[b] : nullptr;
+    p.shadow[b] = in ? L.shadow[b] : nullptr;
+    p.z[b] = in ? L.z[b] : nullptr;
+    p.g[b] = in ? L.g[b] : nullptr;
+  }
+  if (L.io_bf16) {
+    const unsigned blocks = unsigned(L.count) * unsigned(p.mt) * unsigned(p.ntl);
+    hipLaunchKernelGGL((write_mfma_kernel<ST>), dim3(blocks), dim3(256), 0, stream, p);
+  } else {
+    const size_t per_owner = size_t(L.d_ff) * (L.d_model / 4);
+    const unsigned bx = unsigned((per_owner + 255) / 256);
+    hipLaunchKernelGGL((write_valu_kernel<ST>), dim3(bx, L.count), dim3(256), 0, stream, p);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+ReadGeometry read_geometry(int d_ff, int d_model, int state_bf16, int max_group) {
+  ReadGeometry g;
+  const int tile = read_tile_n(state_bf16);
+  g.ks = (d_ff + kReadChunk - 1) / kReadChunk;
+  g.nt = (d_model + tile - 1) / tile;
+  g.npad = g.nt * tile;
+  g.part_floats = size_t(max_group) * g.ks * g.npad;
+  g.total_bytes = (g.part_floats * sizeof(float) + 255) / 256 * 256;
+  return g;
+}
+
+hipError_t launch_read(const ReadLaunch& L, hipStream_t stream) {
+  if (L.io_bf16) {
+    return L.state_bf16 ? launch_read_t<uint16_t, uint16_t>(L, stream)
+                        : launch_read_t<uint16_t, float>(L, stream);
+  }
+  return L.state_bf16 ? launch_read_t<float, uint16_t>(L, stream)
+                      : launch_read_t<float, float>(L, stream);
+}
+
+hipError_t launch_write(const WriteLaunch& L, hipStream_t stream) {
+  return L.state_bf16 ? launch_write_t<uint16_t>(L, stream) : launch_write_t<float>(L, stream);
+}
+
+}  // namespace rwttt

@@ -1,0 +1,188 @@
+"""Serving loop of Algorithm 1 on top of the C ABI, with torch as the allocator.
+
+``Session`` owns the device memory of one workload -- W0 per layer, two state
+slots per (owner, layer) and the library workspace -- and runs decode steps:
+View (committed versions) -> events -> rwttt_plan -> per layer, per group:
+rwttt_read (the step's token) and, for WRITE groups, rwttt_write -> commit or
+rollback of the WRITE owners.  Host code here only marshals arguments; every
+number is computed by the library's kernels.
+"""
+
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+from . import _rwttt as R
+from rwttt_inputs import READ, WRITE, shape_class
+
+TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
+CODE = {"f32": R.RWTTT_F32, "bf16": R.RWTTT_BF16}
+
+
+def to_device(a, dtype, device="cuda", out=None):
+    """Copy a host array (float32, or bf16 bit patterns as uint16) to the device."""
+    if dtype == "bf16":
+        host = torch.from_numpy(np.ascontiguousarray(a).view(np.int16))
+        if out is None:
+            out = torch.empty(host.shape, dtype=torch.bfloat16, device=device)
+        out.view(torch.int16).copy_(host)
+        return out
+    host = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    if out is None:
+        out = torch.empty(host.shape, dtype=torch.float32, device=device)
+    out.copy_(host)
+    return out
+
+
+def to_host(t, dtype):
+    """Device tensor -> host array in the input module's representation."""
+    if dtype == "bf16":
+        return t.detach().view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.detach().float().cpu().numpy()
+
+
+@dataclass
+class StepResult:
+    plan: R.PlanResult
+    committed: list
+    rolled_back: list
+    statuses: list
+
+
+class Session:
+    """Device-resident state of one workload plus the serving loop."""
+
+    def __init__(self, wl, src=None, layers=None, max_group=None, device="cuda",
+                 init_state=True, init_w0=True):
+        self.wl = wl
+        self.device = device
+        self.layers = list(range(wl.n_layers)) if layers is None else list(layers)
+        self.L = len(self.layers)
+        sdt, iodt = TORCH_DTYPE[wl.state_dtype], TORCH_DTYPE[wl.io_dtype]
+        K, N = wl.d_ff, wl.d_model
+        self.w0 = [torch.empty((K, N), dtype=iodt, device=device) for _ in self.layers]
+        self.slots = [[[torch.empty((K, N), dtype=sdt, device=device) for _ in range(2)]
+                       for _ in self.layers] for _ in range(wl.n_owners)]
+        if src is not None and init_w0:
+            for i, l in enumerate(self.layers):
+                to_device(src.w0(l), wl.io_dtype, device, out=self.w0[i])
+        if src is not None and init_state:
+            for r in range(wl.n_owners):
+                for i, l in enumerate(self.layers):
+                    to_device(src.dw_init(r, l), wl.state_dtype, device, out=self.slots[r][i][0])
+        self.max_group = max_group or min(R.RWTTT_MAX_GROUP, wl.n_owners)
+        slot_ptrs = []
+        for r in range(wl.n_owners):
+            for i in range(self.L):
+                slot_ptrs += [self.slots[r][i][0].data_ptr(), self.slots[r][i][1].data_ptr()]
+        cfg = R.make_config(wl.n_owners, self.L, K, N, CODE[wl.io_dtype], CODE[wl.state_dtype],
+                            self.max_group, [w.data_ptr() for w in self.w0], slot_ptrs)
+        ws_bytes = R.rwttt_workspace_bytes(cfg)
+        self.workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=device)
+        cfg.workspace = self.workspace.data_ptr()
+        cfg.workspace_bytes = ws_bytes
+        self.cfg = cfg
+        self.ctx = R.rwttt_create(cfg)
+
+    def close(self):
+        if self.ctx:
+            R.rwttt_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ---- owner table views -------------------------------------------------
+    def version(self, r):
+        return R.rwttt_version(self.ctx, r)
+
+    def versions(self):
+        return [R.rwttt_version(self.ctx, r)[0] for r in range(self.wl.n_owners)]
+
+    def live(self, r, li):
+        """Live slot tensor of owner r at local layer index li."""
+        ptr = R.rwttt_slot(self.ctx, r, li, 0)
+        a, b = self.slots[r][li]
+        return a if a.data_ptr() == ptr else b
+
+    def shadow(self, r, li):
+        ptr = R.rwttt_slot(self.ctx, r, li, 1)
+        a, b = self.slots[r][li]
+        return a if a.data_ptr() == ptr else b
+
+    # ---- one decode step (Algorithm 1) ------------------------------------
+    def events(self, t, items):
+        evs = []
+        for it in items:
+            v, _ = R.rwttt_version(self.ctx, it.owner)
+            evs.append((it.owner, 0, shape_class(self.wl, it.effect, it.chunk), 0,
+                        it.effect, v, t))
+        return evs
+
+    def step(self, t, items, x_ptrs, y_ptrs, zg_ptrs, stream=0, fail_hook=None, timer=None):
+        """Run one step.
+
+        x_ptrs[i], y_ptrs[i]: device addresses of [n_owners, d_ff] inputs and
+        [n_owners, d_model] outputs of local layer i.  zg_ptrs[r] =
+        (z_ptrs_per_layer, g_ptrs_per_layer) for each WRITE owner r.
+        ``timer``, if given, has begin(kind, count, chunk) / end() called
+        around every launch (kind "read" or "write") on the same stream.
+        """
+        wl = self.wl
+        by_owner = {it.owner: it for it in items}
+        plan = R.rwttt_plan(self.ctx, self.events(t, items), t)
+        if plan.status != R.RWTTT_OK:
+            raise R.RwtttError(plan.status, "rwttt_plan")
+        statuses = []
+        write_groups = []
+        for gi in range(plan.n_groups):
+            g = plan.group(gi)
+            owners = plan.owners(gi)
+            emit = any(by_owner[r].emit for r in owners)
+            is_write = g.effect == WRITE
+            chunk = by_owner[owners[0]].chunk if is_write else 0
+            failed = False
+            for i in range(self.L):
+                if emit:
+                    if timer is not None:
+                        timer.begin("read", g.count, 0)
+                    st = R.rwttt_read(self.ctx, g, plan.owner_map_c, i, x_ptrs[i], y_ptrs[i], stream)
+                    if timer is not None:
+                        timer.end()
+                    if st != R.RWTTT_OK:
+                        raise R.RwtttError(st, "rwttt_read")
+                if is_write and not failed:
+                    zs = [zg_ptrs[r][0][i] for r in owners]
+                    gs = [zg_ptrs[r][1][i] for r in owners]
+                    if timer is not None:
+                        timer.begin("write", g.count, chunk)
+                    st = R.rwttt_write(self.ctx, g, plan.owner_map_c, i, chunk, zs, gs, wl.eta, stream)
+                    if timer is not None:
+                        timer.end()
+                    statuses.append(st)
+                    if st != R.RWTTT_OK:
+                        failed = True
+            if is_write:
+                write_groups.append((owners, failed))
+        committed, rolled = [], []
+        for owners, failed in write_groups:
+            # the failure branch of Algorithm 1 rolls a failed group back;
+            # otherwise each owner commits unless its WRITE is declared failed
+            bad = owners if failed else [r for r in owners if by_owner[r].fail or
+                                         (fail_hook is not None and fail_hook(t, r))]
+            good = [r for r in owners if r not in bad]
+            if good:
+                st = R.rwttt_commit(self.ctx, good)
+                if st != R.RWTTT_OK:
+                    raise R.RwtttError(st, "rwttt_commit")
+            if bad:
+                st = R.rwttt_rollback(self.ctx, bad)
+                if st != R.RWTTT_OK:
+                    raise R.RwtttError(st, "rwttt_rollback")
+            committed += good
+            rolled += bad
+        return StepResult(plan, committed, rolled, statuses)

@@ -1,0 +1,264 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Tolerances (written where they are used):
+  * plans, owner maps, versions: bit-exact;
+  * fp32 state: relative Frobenius error <= 1e-3 (after up to 16 WRITEs);
+  * bf16 outputs: max_i |a-b| / max(|b|, 1e-2 rms(b)) <= 2e-2;
+  * fp32 outputs (tiny fp32 workload): the same metric <= 1e-4.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from rwttt_inputs import READ, WRITE, TensorSource, build_trace, workload, draw
+from tests.gpu_util import (R, Session, all_slot_hashes, host_f64, read_group, say, slot_hash,
+                            small_workload, to_device, to_host, write_group)
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+BF16_OUT_TOL = 2e-2
+F32_OUT_TOL = 1e-4
+STATE_TOL = 1e-3
+
+
+def out_tol(dtype):
+    return BF16_OUT_TOL if dtype == "bf16" else F32_OUT_TOL
+
+
+# --------------------------------------------------------------------------
+# whole tiny trace
+# --------------------------------------------------------------------------
+
+def run_gpu_trace(wl, trace, src, steps, layers=None, cols=None, fail_hook=None):
+    layers = list(range(wl.n_layers)) if layers is None else list(layers)
+    sess = Session(wl, src, layers)
+    out = []
+    tdt = torch.float32 if wl.io_dtype == "f32" else torch.bfloat16
+    for t in steps:
+        items = trace[t]
+        X = [to_device(src.x_step(t)[:, l], wl.io_dtype) for l in layers]
+        Y = [torch.zeros((wl.n_owners, wl.d_model), dtype=tdt, device="cuda") for _ in layers]
+        keep, zg = [], {}
+        for it in items:
+            if it.effect == WRITE:
+                Z, G = src.zg_owner(t, it.owner, it.chunk)
+                zd = [to_device(Z[l], wl.io_dtype) for l in layers]
+                gd = [to_device(G[l], wl.io_dtype) for l in layers]
+                keep += zd + gd
+                zg[it.owner] = ([z.data_ptr() for z in zd], [g.data_ptr() for g in gd])
+        res = sess.step(t, items, [x.data_ptr() for x in X], [y.data_ptr() for y in Y], zg,
+                        torch.cuda.current_stream().cuda_stream, fail_hook)
+        torch.cuda.synchronize()
+        ys = {}
+        for it in items:
+            if it.emit:
+                for i, l in enumerate(layers):
+                    row = host_f64(Y[i][it.owner], wl.io_dtype)
+                    ys[(it.owner, l)] = row if cols is None else row[cols]
+        out.append((res, sess.versions(), ys))
+    return sess, out
+
+
+def plan_tuples(res):
+    p = res.plan
+    return [((p.group(i).effect, p.group(i).backend_type, p.group(i).shape_class,
+              p.group(i).placement), p.owners(i)) for i in range(p.n_groups)]
+
+
+def test_tiny_trace_matches_oracle():
+    wl = workload(0)
+    trace, src = build_trace(wl), TensorSource(wl)
+    say("tiny trace", wl.name)
+    snaps = {}
+    ref, table = O.run_trace(wl, trace, src,
+                             on_step=lambda rec, tb: snaps.__setitem__(rec.step, None))
+    sess, got = run_gpu_trace(wl, trace, src, range(wl.n_steps))
+    for rec, (res, versions, ys) in zip(ref, got):
+        assert plan_tuples(res) == [(g.key, g.owners) for g in rec.plan.groups]
+        assert versions == rec.versions
+        for k, v in rec.y.items():
+            assert O.max_rel_floor(ys[k], v) <= F32_OUT_TOL, (rec.step, k)
+    for r in range(wl.n_owners):
+        live = host_f64(sess.live(r, 0), wl.state_dtype)
+        assert O.rel_frobenius(live, table.D[(r, 0)]) <= STATE_TOL
+    assert sess.versions() == [4, 3]
+
+
+# --------------------------------------------------------------------------
+# READ at small and ragged shapes
+# --------------------------------------------------------------------------
+
+READ_CASES = [
+    # d_ff, d_model, io, state, n_owners, group
+    (256, 64, "f32", "f32", 2, [1, 0]),
+    (1000, 264, "bf16", "f32", 12, [3, 0, 7, 11, 5]),
+    (1000, 264, "bf16", "bf16", 12, [2, 9, 4, 0, 1, 6, 8, 10, 11]),
+    (520, 1032, "bf16", "f32", 20, list(range(19, -1, -1))[:17]),
+    (264, 520, "f32", "bf16", 3, [2]),
+    (9728, 2560, "bf16", "f32", 8, list(range(8))),
+]
+
+
+@pytest.mark.parametrize("d_ff,d_model,io,state,n_owners,group", READ_CASES)
+def test_read_matches_oracle(d_ff, d_model, io, state, n_owners, group):
+    wl = small_workload(d_ff, d_model, io, state, n_owners)
+    say("read", d_ff, d_model, io, state, group)
+    src = TensorSource(wl)
+    sess = Session(wl, src)
+    X = draw((n_owners, d_ff), 1.0, io, wl.seed, (77, 1))
+    xd = to_device(X, io)
+    tdt = torch.float32 if io == "f32" else torch.bfloat16
+    before = all_slot_hashes(sess)
+    y = torch.zeros((n_owners, d_model), dtype=tdt, device="cuda")
+    read_group(sess, group, 0, xd, y)
+    torch.cuda.synchronize()
+    W0 = O.widen(src.w0(0), io)
+    for r in group:
+        ref = O.round_to(O.read_apply(O.widen(X[r], io), W0, O.widen(src.dw_init(r, 0), state)), io)
+        assert O.max_rel_floor(host_f64(y[r], io), ref) <= out_tol(io), r
+    # READ leaves every slot and version untouched
+    assert all_slot_hashes(sess) == before
+    assert sess.versions() == [0] * n_owners
+    # rows outside the group are not written
+    others = [r for r in range(n_owners) if r not in group]
+    if others:
+        assert torch.count_nonzero(y[others].float()).item() == 0
+    # batched == sequential and owner order: bit-identical rows
+    y1 = torch.zeros_like(y)
+    for r in group:
+        read_group(sess, [r], 0, xd, y1)
+    y2 = torch.zeros_like(y)
+    read_group(sess, list(reversed(group)), 0, xd, y2)
+    torch.cuda.synchronize()
+    assert torch.equal(y[group].view(torch.int16 if io == "bf16" else torch.int32),
+                       y1[group].view(torch.int16 if io == "bf16" else torch.int32))
+    assert torch.equal(y[group], y2[group])
+
+
+# --------------------------------------------------------------------------
+# WRITE, commit, rollback at small and ragged shapes
+# --------------------------------------------------------------------------
+
+WRITE_CASES = [
+    # d_ff, d_model, io, state, chunk, group
+    (256, 64, "f32", "f32", 4, [0, 1]),
+    (1000, 264, "bf16", "f32", 1, [2]),
+    (1000, 264, "bf16", "f32", 17, [0, 3, 1]),
+    (1000, 264, "bf16", "bf16", 64, [1, 2]),
+    (520, 1032, "bf16", "f32", 100, [3, 0]),
+    (128, 64, "bf16", "f32", 32, [0, 1, 2, 3]),
+    (9728, 2560, "bf16", "f32", 64, [1]),
+]
+
+
+@pytest.mark.parametrize("d_ff,d_model,io,state,chunk,group", WRITE_CASES)
+def test_write_commit_rollback_match_oracle(d_ff, d_model, io, state, chunk, group):
+    n_owners = 4
+    wl = small_workload(d_ff, d_model, io, state, n_owners, eta=0.05)
+    say("write", d_ff, d_model, io, state, chunk, group)
+    src = TensorSource(wl)
+    sess = Session(wl, src)
+    zs, gs, ref = [], [], {}
+    for r in group:
+        Z = draw((chunk, d_ff), 1.0, io, wl.seed, (78, r), absval=True)
+        G = draw((chunk, d_model), 1.0, io, wl.seed, (79, r))
+        zs.append(to_device(Z, io))
+        gs.append(to_device(G, io))
+        ref[r] = O.round_to(O.write_candidate(O.widen(src.dw_init(r, 0), state), O.widen(Z, io),
+                                              O.widen(G, io), wl.eta), state)
+    before = all_slot_hashes(sess)
+    st = write_group(sess, group, 0, chunk, zs, gs)
+    assert st == R.RWTTT_OK, R.rwttt_strerror(st)
+    torch.cuda.synchronize()
+    after = all_slot_hashes(sess)
+    # only the group's shadow slots changed
+    for key in before:
+        r, i, s = key
+        if r in group and s == 1:
+            continue
+        assert after[key] == before[key], key
+    for r in group:
+        shadow = host_f64(sess.shadow(r, 0), state)
+        if state == "f32":
+            assert O.rel_frobenius(shadow, ref[r]) <= STATE_TOL
+        else:
+            assert O.max_rel_floor(shadow, ref[r]) <= BF16_OUT_TOL
+        assert sess.version(r) == (0, True)
+    # roll back the first owner, commit the rest
+    keep_live = slot_hash(sess.live(group[0], 0))
+    assert R.rwttt_rollback(sess.ctx, [group[0]]) == R.RWTTT_OK
+    assert slot_hash(sess.live(group[0], 0)) == keep_live
+    assert sess.version(group[0]) == (0, False)
+    if len(group) > 1:
+        shadow_hash = {r: slot_hash(sess.shadow(r, 0)) for r in group[1:]}
+        assert R.rwttt_commit(sess.ctx, group[1:]) == R.RWTTT_OK
+        for r in group[1:]:
+            assert sess.version(r) == (1, False)
+            assert slot_hash(sess.live(r, 0)) == shadow_hash[r]
+
+
+def test_injected_write_failure_rolls_back_exactly():
+    wl = small_workload(520, 264, "bf16", "f32", 3)
+    src = TensorSource(wl)
+    sess = Session(wl, src)
+    say("inject failure")
+    z = [to_device(draw((16, 520), 1.0, "bf16", 1, (1,)), "bf16")]
+    g = [to_device(draw((16, 264), 1.0, "bf16", 1, (2,)), "bf16")]
+    live = slot_hash(sess.live(1, 0))
+    assert R.rwttt_inject_write_failures(sess.ctx, 1) == R.RWTTT_OK
+    assert write_group(sess, [1], 0, 16, z, g) == R.RWTTT_E_WRITE_FAILED
+    assert R.rwttt_commit(sess.ctx, [1]) == R.RWTTT_E_WRITE_FAILED
+    assert R.rwttt_rollback(sess.ctx, [1]) == R.RWTTT_OK
+    torch.cuda.synchronize()
+    assert slot_hash(sess.live(1, 0)) == live and sess.version(1) == (0, False)
+    # the owner writes normally afterwards
+    assert write_group(sess, [1], 0, 16, z, g) == R.RWTTT_OK
+    assert R.rwttt_commit(sess.ctx, [1]) == R.RWTTT_OK
+    assert sess.version(1) == (1, False)
+
+
+# --------------------------------------------------------------------------
+# full shapes, in the launch configuration of the benchmark
+# --------------------------------------------------------------------------
+
+def test_sixteen_writes_fp32_state_full_shape():
+    """16 consecutive WRITE+commit of one owner at d_ff 9728, d_model 2560, C 64."""
+    import dataclasses
+    wl = dataclasses.replace(workload(2), n_owners=1, n_layers=1)
+    src = TensorSource(wl)
+    say("16 writes full shape")
+    sess = Session(wl, src)
+    D = O.widen(src.dw_init(0, 0), "f32")
+    for t in range(16):
+        Z, G = src.zg(t, 0, 0, 64)
+        st = write_group(sess, [0], 0, 64, [to_device(Z, "bf16")], [to_device(G, "bf16")])
+        assert st == R.RWTTT_OK
+        assert R.rwttt_commit(sess.ctx, [0]) == R.RWTTT_OK
+        D = O.round_to(O.write_candidate(D, O.widen(Z, "bf16"), O.widen(G, "bf16"), wl.eta), "f32")
+    torch.cuda.synchronize()
+    err = O.rel_frobenius(host_f64(sess.live(0, 0), "f32"), D)
+    say("rel frobenius after 16 writes", err)
+    assert err <= STATE_TOL
+    assert sess.version(0) == (16, False)
+
+
+def test_read8_full_shape_matches_oracle():
+    """Eight owners at d_ff 9728, d_model 2560: bf16 io, fp32 state."""
+    wl = workload(1)
+    src = TensorSource(wl)
+    say("read8 full shape")
+    sess = Session(wl, src)
+    W0 = O.widen(src.w0(0), "bf16")
+    D = [O.widen(src.dw_init(r, 0), "f32") for r in range(8)]
+    y = torch.zeros((8, wl.d_model), dtype=torch.bfloat16, device="cuda")
+    for t in range(2):
+        X = src.x_step(t)[:, 0]
+        read_group(sess, list(range(8)), 0, to_device(X, "bf16"), y)
+        torch.cuda.synchronize()
+        for r in range(8):
+            ref = O.round_to(O.read_apply(O.widen(X[r], "bf16"), W0, D[r]), "bf16")
+            err = O.max_rel_floor(host_f64(y[r], "bf16"), ref)
+            assert err <= BF16_OUT_TOL, (t, r, err)

@@ -1,0 +1,180 @@
+"""Host-side checks of the C ABI that need no GPU.
+
+The library loads on a machine without a GPU; planning, the owner table and
+every validation path run on the host.  A context without workspace never
+touches the device, and the fake slot addresses below are never dereferenced.
+"""
+
+import os
+import random
+import re
+import subprocess
+
+import pytest
+
+import oracle as O
+
+R = pytest.importorskip("paper_2605_28053_amd._rwttt",
+                        reason="librwttt.so not built (python -m paper_2605_28053_amd.build)")
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rwttt.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rwttt_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) == 13
+    out = subprocess.run(["nm", "-D", "--defined-only", R.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (rwttt_\w+)", out))
+    for n in names:
+        assert n in exported, n
+        assert hasattr(R.lib(), n)
+
+
+def host_ctx(n_owners=6, n_layers=2, d_ff=64, d_model=32, max_group=8):
+    w0 = [0x10000 * (i + 1) for i in range(n_layers)]
+    slots = [0x1000000 + 0x1000 * i for i in range(n_owners * n_layers * 2)]
+    cfg = R.make_config(n_owners, n_layers, d_ff, d_model, R.RWTTT_BF16, R.RWTTT_F32,
+                        max_group, w0, slots)
+    return R.rwttt_create(cfg), cfg
+
+
+def make_dirty(ctx, owners, layer=0):
+    """Open a (failed) candidate for owners without touching the device."""
+    g = R.make_group(R.RWTTT_WRITE, 0, len(owners))
+    assert R.rwttt_inject_write_failures(ctx, 1) == R.RWTTT_OK
+    st = R.rwttt_write(ctx, g, R.u32_array(owners), layer, 4, [0x100] * len(owners),
+                       [0x200] * len(owners), 1.0)
+    assert st == R.RWTTT_E_WRITE_FAILED
+
+
+def test_plan_matches_oracle_planner_bit_exactly():
+    rng = random.Random(11)
+    for trial in range(400):
+        n_owners = rng.randint(1, 12)
+        ctx, _ = host_ctx(n_owners=n_owners)
+        dirty = [rng.random() < 0.2 for _ in range(n_owners)]
+        d_owners = [r for r in range(n_owners) if dirty[r]]
+        if d_owners:
+            make_dirty(ctx, d_owners)
+        step = rng.randint(0, 6)
+        B = rng.choice([0, 0, 1, 2, 3, 5])
+        w = rng.choice([0, 0, 1, 2, 4])
+        owners = rng.sample(range(n_owners + 2), rng.randint(0, n_owners))
+        events = []
+        for r in owners:
+            events.append((r, rng.choice([0, 1]), rng.choice([0, 3, 9]), rng.choice([0, 1]),
+                           rng.choice([0, 1, 1, 1, 2]), rng.choice([0, 0, 0, 1]),
+                           rng.randint(0, step + 1)))
+        if owners and rng.random() < 0.05:
+            events.append(events[0])          # alias
+        p = R.rwttt_plan(ctx, events, step, B, w)
+        oe = [O.Event(r, tau, sig, pi, eff, v, rd) for (r, tau, sig, pi, eff, v, rd) in events]
+        q = O.plan(oe, [0] * n_owners, dirty, n_owners, step, B, w)
+        assert p.status == q.status
+        assert p.ev_status == q.ev_status
+        if q.status == O.OK:
+            got = [((p.group(i).effect, p.group(i).backend_type, p.group(i).shape_class,
+                     p.group(i).placement), p.owners(i)) for i in range(p.n_groups)]
+            assert got == [(g.key, g.owners) for g in q.groups]
+            assert p.deferred == q.deferred
+        R.rwttt_destroy(ctx)
+
+
+def test_plan_capacity_reports_needed_sizes():
+    ctx, _ = host_ctx()
+    events = [(r, 0, 0, 0, r % 2, 0, 0) for r in range(6)]
+    p = R.rwttt_plan(ctx, events, 0, cap=1)
+    assert p.status == R.RWTTT_E_CAPACITY
+    assert (p.n_groups, p.n_mapped) == (2, 6)
+    p = R.rwttt_plan(ctx, events, 0)
+    assert p.status == R.RWTTT_OK and [p.owners(i) for i in range(2)] == [[0, 2, 4], [1, 3, 5]]
+
+
+def test_owner_table_state_machine_and_error_codes():
+    ctx, _ = host_ctx(n_owners=4)
+    # commit / rollback of a clean owner
+    assert R.rwttt_commit(ctx, [0]) == R.RWTTT_E_NOT_DIRTY
+    assert R.rwttt_rollback(ctx, [0]) == R.RWTTT_E_NOT_DIRTY
+    assert R.rwttt_commit(ctx, [9]) == R.RWTTT_E_INVALID
+    # a WRITE needs a WRITE group
+    rg = R.make_group(R.RWTTT_READ, 0, 1)
+    assert R.rwttt_write(ctx, rg, R.u32_array([1]), 0, 4, [0x100], [0x200], 1.0) == R.RWTTT_E_KEY_MISMATCH
+    # failed WRITE: dirty, cannot commit, plan rejects, rollback restores
+    live0 = R.rwttt_slot(ctx, 1, 0, 0)
+    make_dirty(ctx, [1, 2])
+    assert R.rwttt_version(ctx, 1) == (0, True)
+    assert R.rwttt_commit(ctx, [1]) == R.RWTTT_E_WRITE_FAILED
+    p = R.rwttt_plan(ctx, [(1, 0, 0, 0, 0, 0, 0), (3, 0, 0, 0, 0, 0, 0)], 0)
+    assert p.ev_status == [R.RWTTT_E_DIRTY, R.RWTTT_OK]
+    # aliasing is checked before anything changes
+    assert R.rwttt_rollback(ctx, [1, 1]) == R.RWTTT_E_OWNER_ALIAS
+    assert R.rwttt_rollback(ctx, [1, 3]) == R.RWTTT_E_NOT_DIRTY
+    assert R.rwttt_version(ctx, 1) == (0, True)
+    assert R.rwttt_rollback(ctx, [1, 2]) == R.RWTTT_OK
+    assert R.rwttt_version(ctx, 1) == (0, False)
+    assert R.rwttt_slot(ctx, 1, 0, 0) == live0
+    # the same layer cannot be written twice in one open transition
+    make_dirty(ctx, [0], layer=1)
+    wg = R.make_group(R.RWTTT_WRITE, 0, 1)
+    assert R.rwttt_write(ctx, wg, R.u32_array([0]), 1, 4, [0x100], [0x200], 1.0) == R.RWTTT_E_WRITE_FAILED
+    assert R.rwttt_rollback(ctx, [0]) == R.RWTTT_OK
+    # no workspace: device calls are refused, nothing is launched
+    assert R.rwttt_read(ctx, rg, R.u32_array([0]), 0, 0x1000, 0x2000) == R.RWTTT_E_INVALID
+    empty = R.make_group(R.RWTTT_READ, 0, 0)
+    assert R.rwttt_read(ctx, empty, R.u32_array([]), 0, 0x1000, 0x2000) == R.RWTTT_OK
+    # bad layer, alias inside a group
+    assert R.rwttt_read(ctx, rg, R.u32_array([0]), 5, 0x1000, 0x2000) == R.RWTTT_E_INVALID
+    ag = R.make_group(R.RWTTT_READ, 0, 2)
+    assert R.rwttt_read(ctx, ag, R.u32_array([2, 2]), 0, 0x1000, 0x2000) == R.RWTTT_E_OWNER_ALIAS
+
+
+def test_slots_are_live_and_shadow_of_each_owner_layer():
+    ctx, cfg = host_ctx(n_owners=3, n_layers=2)
+    for r in range(3):
+        for l in range(2):
+            base = 0x1000000 + 0x1000 * ((r * 2 + l) * 2)
+            assert R.rwttt_slot(ctx, r, l, 0) == base
+            assert R.rwttt_slot(ctx, r, l, 1) == base + 0x1000
+
+
+def test_create_rejects_bad_configs():
+    ok = dict(n_owners=2, n_layers=1, d_ff=64, d_model=32, io_dtype=1, state_dtype=0, max_group=2)
+
+    def make(**kw):
+        a = dict(ok)
+        a.update(kw)
+        slots = kw.pop("_slots", None) or [0x1000000 + 0x1000 * i for i in range(a["n_owners"] * a["n_layers"] * 2)]
+        cfg = R.make_config(a["n_owners"], a["n_layers"], a["d_ff"], a["d_model"], a["io_dtype"],
+                            a["state_dtype"], a["max_group"], [0x10000] * a["n_layers"], slots)
+        return cfg
+
+    for bad in [dict(d_ff=60), dict(d_model=12), dict(max_group=0), dict(max_group=65),
+                dict(io_dtype=3), dict(n_owners=0)]:
+        with pytest.raises(R.RwtttError) as e:
+            R.rwttt_create(make(**bad))
+        assert e.value.status == R.RWTTT_E_INVALID
+    dup = make()
+    dup.slots[1] = dup.slots[0]
+    with pytest.raises(R.RwtttError) as e:
+        R.rwttt_create(dup)
+    assert e.value.status == R.RWTTT_E_OWNER_ALIAS
+    small = make()
+    small.workspace = 0x100000000
+    small.workspace_bytes = 16
+    with pytest.raises(R.RwtttError) as e:
+        R.rwttt_create(small)
+    assert e.value.status == R.RWTTT_E_CAPACITY
+
+
+def test_strerror_covers_every_code():
+    for code in range(-9, 2):
+        assert R.rwttt_strerror(code) != "unknown status"
+    assert R.rwttt_strerror(-42) == "unknown status"
