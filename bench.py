@@ -39,6 +39,33 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def measured_traffic(records):
+    """Mean HBM bytes per READ call from the committed rocprofv3 PMC summary.
+
+    The summary holds FETCH_SIZE and WRITE_SIZE per dispatch, scaled by what
+    the same counters read for a plain 1 GiB device copy.  It is used only if
+    the kernel source is the one the counters were taken on; else None.
+    """
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "hbm_traffic__mixed8-4b-36L.json")
+    src = os.path.join(ROOT, "paper_2605_28053_amd", "csrc", "rwttt_kernels.hip")
+    try:
+        summ = json.load(open(path))
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    if summ.get("kernel_source_sha256") != sha:
+        return None
+    table = summ["read_call_bytes_by_group_size"]
+    tot = 0.0
+    for _, b, _, _, _ in records:
+        e = table.get(str(b))
+        if e is None:
+            return None
+        tot += e["fetch"] + e["write"]
+    return tot / len(records)
+
+
 class LaunchTimer:
     """HIP events around every launch, on torch's current stream."""
 
@@ -74,7 +101,7 @@ class LaunchTimer:
                 byt = sum(b * (2 * st * K * N + io * c * (K + N)) for _, b, c, _, _ in recs)
                 flop = sum(2.0 * b * c * K * N for _, b, c, _, _ in recs)
             out[kind] = dict(launches=len(recs), total_ms=ms, avg_us=1e3 * ms / len(recs),
-                             bytes=byt, flops=flop,
+                             bytes=byt, flops=flop, records=recs,
                              gbs=byt / (ms * 1e-3) / 1e9, tflops=flop / (ms * 1e-3) / 1e12)
         return out
 
@@ -211,6 +238,8 @@ def main():
     ap.add_argument("--cpu-steps", type=int, default=30)
     ap.add_argument("--cpu-layers", type=int, nargs="+", default=[0, 1])
     ap.add_argument("--kernel-events", choices=["on", "off"], default="on")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="only run 5 plain device copies of BYTES each (HBM counter calibration)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -224,6 +253,15 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    if args.calibrate_copy:
+        # A plain copy of known size: reads and writes exactly BYTES per launch.
+        a = torch.ones(args.calibrate_copy // 4, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": args.calibrate_copy, "launches": 5}))
+        return
     from rwttt_inputs import workload
     wl = workload(2)
     layers = list(range(wl.n_layers if args.layers is None else args.layers))
@@ -256,10 +294,13 @@ def main():
     }
     if "read" in kern:
         rd = kern["read"]
-        line["roofline"] = {"bound": "hbm", "kernel": "read_kernel",
+        traffic = measured_traffic(rd["records"])
+        line["roofline"] = {"bound": "hbm", "kernel": "read_partial_kernel+read_reduce_kernel",
                             "achieved": round(rd["gbs"], 1), "peak": HBM_PEAK_GBS,
                             "unit": "GB/s", "frac": round(rd["gbs"] / HBM_PEAK_GBS, 4),
-                            "traffic": None, "avg_launch_us": round(rd["avg_us"], 2),
+                            "traffic": None if traffic is None else round(traffic),
+                            "algorithmic_bytes_per_launch": round(rd["bytes"] / rd["launches"]),
+                            "avg_launch_us": round(rd["avg_us"], 2),
                             "launches": rd["launches"]}
     if "write" in kern:
         wr = kern["write"]

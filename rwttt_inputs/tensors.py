@@ -61,22 +61,40 @@ class TensorSource:
     zg(t, r, l, C)  ([C, d_ff], [C, d_model])  io dtype
     """
 
-    def __init__(self, wl: Workload, cache_steps=True):
+    def __init__(self, wl: Workload, cache_steps=True, memo=False):
         self.wl = wl
         self._xcache = {}
         self._cache_steps = cache_steps
+        self._memo = {} if memo else None
+
+    def _remember(self, key, fn):
+        if self._memo is None:
+            return fn()
+        if key not in self._memo:
+            self._memo[key] = fn()
+        return self._memo[key]
+
+    def prefetch(self, owners, layers, threads=8):
+        """Draw W0 and the initial state of (owners x layers) in parallel (memo only)."""
+        from concurrent.futures import ThreadPoolExecutor
+        assert self._memo is not None, "prefetch needs memo=True"
+        jobs = [("w0", l) for l in layers] + [("dw", r, l) for r in owners for l in layers]
+        with ThreadPoolExecutor(threads) as ex:
+            list(ex.map(lambda j: self.w0(j[1]) if j[0] == "w0" else self.dw_init(j[1], j[2]), jobs))
 
     # ---- shared weights and initial state --------------------------------
     def w0(self, l):
         wl = self.wl
-        return draw((wl.d_ff, wl.d_model), wl.w0_std, wl.io_dtype, wl.seed, (K_W0, l))
+        return self._remember(("w0", l), lambda: draw(
+            (wl.d_ff, wl.d_model), wl.w0_std, wl.io_dtype, wl.seed, (K_W0, l)))
 
     def dw_init(self, r, l):
         wl = self.wl
         if wl.dw_std == 0.0:
             dt = np.float32 if wl.state_dtype == "f32" else np.uint16
             return np.zeros((wl.d_ff, wl.d_model), dtype=dt)
-        return draw((wl.d_ff, wl.d_model), wl.dw_std, wl.state_dtype, wl.seed, (K_DW, r, l))
+        return self._remember(("dw", r, l), lambda: draw(
+            (wl.d_ff, wl.d_model), wl.dw_std, wl.state_dtype, wl.seed, (K_DW, r, l)))
 
     # ---- per-step activations --------------------------------------------
     def x_step(self, t):
@@ -106,5 +124,5 @@ class TensorSource:
         return Z, G
 
     def zg(self, t, r, l, C):
-        Z, G = self.zg_owner(t, r, C)
+        Z, G = self._remember(("zg", t, r, C), lambda: self.zg_owner(t, r, C))
         return Z[l], G[l]

@@ -53,3 +53,45 @@ def write_group(sess, owners, li, chunk, zs, gs, eta=None):
 
 def host_f64(t, dtype):
     return O.widen(to_host(t, dtype), dtype)
+
+
+def run_gpu_trace(wl, trace, src, steps, layers=None, cols=None, fail_hook=None):
+    """Run steps of a trace through Session.step (the serving loop) and collect
+    (StepResult, versions after the step, {(owner, layer): y row}) per step."""
+    layers = list(range(wl.n_layers)) if layers is None else list(layers)
+    sess = Session(wl, src, layers)
+    out = []
+    tdt = torch.float32 if wl.io_dtype == "f32" else torch.bfloat16
+    for t in steps:
+        items = trace[t]
+        X = [to_device(src.x_step(t)[:, l], wl.io_dtype) for l in layers]
+        Y = [torch.zeros((wl.n_owners, wl.d_model), dtype=tdt, device="cuda") for _ in layers]
+        keep, zg = [], {}
+        for it in items:
+            if it.effect == WRITE:
+                zd, gd = [], []
+                for l in layers:
+                    Z, G = src.zg(t, it.owner, l, it.chunk)
+                    zd.append(to_device(Z, wl.io_dtype))
+                    gd.append(to_device(G, wl.io_dtype))
+                keep += zd + gd
+                zg[it.owner] = ([z.data_ptr() for z in zd], [g.data_ptr() for g in gd])
+        res = sess.step(t, items, [x.data_ptr() for x in X], [y.data_ptr() for y in Y], zg,
+                        torch.cuda.current_stream().cuda_stream, fail_hook)
+        torch.cuda.synchronize()
+        ys = {}
+        for it in items:
+            if it.emit:
+                for i, l in enumerate(layers):
+                    row = host_f64(Y[i][it.owner], wl.io_dtype)
+                    ys[(it.owner, l)] = row if cols is None else row[cols]
+        out.append((res, sess.versions(), ys))
+    return sess, out
+
+
+def plan_tuples(res):
+    p = res.plan
+    return [((p.group(i).effect, p.group(i).backend_type, p.group(i).shape_class,
+              p.group(i).placement), p.owners(i)) for i in range(p.n_groups)]
+
+

@@ -13,8 +13,9 @@ import torch
 
 import oracle as O
 from rwttt_inputs import READ, WRITE, TensorSource, build_trace, workload, draw
-from tests.gpu_util import (R, Session, all_slot_hashes, host_f64, read_group, say, slot_hash,
-                            small_workload, to_device, to_host, write_group)
+from tests.gpu_util import (R, Session, all_slot_hashes, host_f64, plan_tuples, read_group,
+                            run_gpu_trace, say, slot_hash, small_workload, to_device, to_host,
+                            write_group)
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
@@ -31,42 +32,6 @@ def out_tol(dtype):
 # --------------------------------------------------------------------------
 # whole tiny trace
 # --------------------------------------------------------------------------
-
-def run_gpu_trace(wl, trace, src, steps, layers=None, cols=None, fail_hook=None):
-    layers = list(range(wl.n_layers)) if layers is None else list(layers)
-    sess = Session(wl, src, layers)
-    out = []
-    tdt = torch.float32 if wl.io_dtype == "f32" else torch.bfloat16
-    for t in steps:
-        items = trace[t]
-        X = [to_device(src.x_step(t)[:, l], wl.io_dtype) for l in layers]
-        Y = [torch.zeros((wl.n_owners, wl.d_model), dtype=tdt, device="cuda") for _ in layers]
-        keep, zg = [], {}
-        for it in items:
-            if it.effect == WRITE:
-                Z, G = src.zg_owner(t, it.owner, it.chunk)
-                zd = [to_device(Z[l], wl.io_dtype) for l in layers]
-                gd = [to_device(G[l], wl.io_dtype) for l in layers]
-                keep += zd + gd
-                zg[it.owner] = ([z.data_ptr() for z in zd], [g.data_ptr() for g in gd])
-        res = sess.step(t, items, [x.data_ptr() for x in X], [y.data_ptr() for y in Y], zg,
-                        torch.cuda.current_stream().cuda_stream, fail_hook)
-        torch.cuda.synchronize()
-        ys = {}
-        for it in items:
-            if it.emit:
-                for i, l in enumerate(layers):
-                    row = host_f64(Y[i][it.owner], wl.io_dtype)
-                    ys[(it.owner, l)] = row if cols is None else row[cols]
-        out.append((res, sess.versions(), ys))
-    return sess, out
-
-
-def plan_tuples(res):
-    p = res.plan
-    return [((p.group(i).effect, p.group(i).backend_type, p.group(i).shape_class,
-              p.group(i).placement), p.owners(i)) for i in range(p.n_groups)]
-
 
 def test_tiny_trace_matches_oracle():
     wl = workload(0)
