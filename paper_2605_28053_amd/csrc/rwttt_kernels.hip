@@ -5,6 +5,8 @@
 //
 // Both operate on groups of owners, one launch per (group, layer).
 
+#include <algorithm>
+
 #include "rwttt_kernels.h"
 
 namespace rwttt {
@@ -375,6 +377,163 @@ __global__ void __launch_bounds__(256) write_mfma_kernel(const WriteParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// WRITE, bf16 evidence, small chunk (C <= 64): streaming rank-C update
+// ---------------------------------------------------------------------------
+//
+// For C <= 64 the update moves 2 x |dW| bytes for only 2C flop per element,
+// so it is HBM-bound and must stream like a copy.  A persistent grid of blocks
+// each keeps one 256-column tile of d_model and walks (owner, 32-row tile)
+// items.  Per owner, each wave loads its two 32-column blocks of G once into
+// MFMA operand registers.  Per item: Z's 32 x C tile is staged through LDS
+// transposed to rank-contiguous rows, eight or fewer MFMAs form
+// D[m][n] = sum_c Z[c][m] G[c][n], the accumulators go through LDS, and every
+// wave reads, updates and stores whole 1 KB rows of the slot while the next
+// item's live rows are already loading.
+
+constexpr int kSTM = 32;                 // rows per item
+constexpr int kSTN = 256;                // columns per tile
+constexpr int kSMaxC = 64;               // largest chunk on this path
+static_assert(kSMaxC * kSTN * 2 <= kSTM * kSTN * 4, "G tile must fit the output buffer");
+constexpr int kSPitch = kSMaxC + 8;      // bf16 per staged Z row (144 B, 16-B aligned)
+constexpr int kSBlocksTarget = 512;      // about two resident blocks per CU
+
+template <typename ST>
+__device__ __forceinline__ void stream_load_rows(const ST* live, int d_ff, int d_model, int m0,
+                                                 int wave, int ncol, bool ncol_ok,
+                                                 Packed<ST, 4> (&lv)[kSTM / 4]) {
+#pragma unroll
+  for (int rr = 0; rr < kSTM / 4; ++rr) {
+    const int m = m0 + wave * (kSTM / 4) + rr;
+    if (m < d_ff && ncol_ok) load_packed<true>(live + size_t(m) * d_model + ncol, lv[rr]);
+    else lv[rr].zero();
+  }
+}
+
+template <typename ST>
+__global__ void __launch_bounds__(256) write_stream_kernel(const WriteParams p) {
+  constexpr int RPW = kSTM / 4;           // epilogue rows per wave
+  constexpr int KSMAX = kSMaxC / 16;      // MFMA k-steps
+  __shared__ __attribute__((aligned(16))) uint16_t zt[kSTM * kSPitch];
+  __shared__ __attribute__((aligned(16))) float out[kSTM * kSTN];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int half = lane >> 5;
+  const int nt = blockIdx.x % p.ntl;
+  const int j0 = blockIdx.x / p.ntl;
+  const int jstep = gridDim.x / p.ntl;
+  const int items = p.count * p.mt;
+  if (j0 >= items) return;
+  const int n0 = nt * kSTN;
+  const int ncol = n0 + lane * 4;
+  const bool ncol_ok = ncol < p.d_model;
+  const int ksteps = (p.chunk + 15) / 16;
+  const float eta = p.eta;
+
+  bf16x8_t gf[2][KSMAX];
+  int cur_b = -1;
+  Packed<ST, 4> lv[RPW];
+  {
+    const int b = j0 / p.mt;
+    stream_load_rows(static_cast<const ST*>(p.live[b]), p.d_ff, p.d_model, (j0 - b * p.mt) * kSTM,
+                     wave, ncol, ncol_ok, lv);
+  }
+  for (int j = j0; j < items; j += jstep) {
+    const int b = j / p.mt;
+    const int m0 = (j - b * p.mt) * kSTM;
+    const uint16_t* Z = static_cast<const uint16_t*>(p.z[b]);
+    if (b != cur_b) {
+      // Stage owner b's G tile [C ranks][256 n] through the idle output buffer,
+      // transposed to gs[n][rank] (64 ranks per row), and keep this wave's two
+      // 32-column blocks as MFMA operands for all of the owner's items.
+      const uint16_t* G = static_cast<const uint16_t*>(p.g[b]);
+      uint16_t* gs = reinterpret_cast<uint16_t*>(out);
+      for (int it = tid; it < (kSMaxC / 2) * (kSTN / 8); it += 256) {
+        const int cp = it >> 5, ng = it & 31;
+        const int nn = n0 + ng * 8, c = 2 * cp;
+        uint4 r0 = make_uint4(0, 0, 0, 0), r1 = make_uint4(0, 0, 0, 0);
+        if (nn < p.d_model) {
+          if (c < p.chunk) r0 = *reinterpret_cast<const uint4*>(G + size_t(c) * p.d_model + nn);
+          if (c + 1 < p.chunk) r1 = *reinterpret_cast<const uint4*>(G + size_t(c + 1) * p.d_model + nn);
+        }
+        const uint32_t a[4] = {r0.x, r0.y, r0.z, r0.w}, bb[4] = {r1.x, r1.y, r1.z, r1.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          *reinterpret_cast<uint32_t*>(&gs[(ng * 8 + 2 * q) * kSMaxC + 2 * cp]) = (a[q] & 0xffffu) | (bb[q] << 16);
+          *reinterpret_cast<uint32_t*>(&gs[(ng * 8 + 2 * q + 1) * kSMaxC + 2 * cp]) = (a[q] >> 16) | (bb[q] & 0xffff0000u);
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int s = 0; s < KSMAX; ++s)
+          gf[i][s] = *reinterpret_cast<const bf16x8_t*>(
+              &gs[((wave * 2 + i) * 32 + (lane & 31)) * kSMaxC + s * 16 + half * 8]);
+      __syncthreads();
+      cur_b = b;
+    }
+    // Z tile [C ranks][32 m] -> zt[m][rank]; 128 threads, 2 ranks x 8 m each
+    if (tid < 128) {
+      const int cp = tid >> 2, mg = tid & 3;
+      const int mm = m0 + mg * 8, c = 2 * cp;
+      uint4 r0 = make_uint4(0, 0, 0, 0), r1 = make_uint4(0, 0, 0, 0);
+      if (mm < p.d_ff) {
+        if (c < p.chunk) r0 = *reinterpret_cast<const uint4*>(Z + size_t(c) * p.d_ff + mm);
+        if (c + 1 < p.chunk) r1 = *reinterpret_cast<const uint4*>(Z + size_t(c + 1) * p.d_ff + mm);
+      }
+      const uint32_t a[4] = {r0.x, r0.y, r0.z, r0.w}, bb[4] = {r1.x, r1.y, r1.z, r1.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        *reinterpret_cast<uint32_t*>(&zt[(mg * 8 + 2 * q) * kSPitch + 2 * cp]) = (a[q] & 0xffffu) | (bb[q] << 16);
+        *reinterpret_cast<uint32_t*>(&zt[(mg * 8 + 2 * q + 1) * kSPitch + 2 * cp]) = (a[q] >> 16) | (bb[q] & 0xffff0000u);
+      }
+    }
+    __syncthreads();
+    f32x16_t acc[2] = {f32x16_t{}, f32x16_t{}};
+#pragma unroll
+    for (int s = 0; s < KSMAX; ++s) {
+      if (s < ksteps) {
+        const bf16x8_t az = *reinterpret_cast<const bf16x8_t*>(&zt[(lane & 31) * kSPitch + s * 16 + half * 8]);
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(az, gf[0][s], acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(az, gf[1][s], acc[1], 0, 0, 0);
+      }
+    }
+    // the next item's live rows load while this one finishes
+    Packed<ST, 4> nx[RPW];
+    const int jn = j + jstep;
+    if (jn < items) {
+      const int bn = jn / p.mt;
+      stream_load_rows(static_cast<const ST*>(p.live[bn]), p.d_ff, p.d_model, (jn - bn * p.mt) * kSTM,
+                       wave, ncol, ncol_ok, nx);
+    }
+    // accumulator register 4q+e of lane l holds D[8q + 4(l/32) + e][l % 32]
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        out[(8 * (r >> 2) + 4 * half + (r & 3)) * kSTN + (wave * 2 + i) * 32 + (lane & 31)] = acc[i][r];
+    __syncthreads();
+    ST* shadow = static_cast<ST*>(p.shadow[b]);
+#pragma unroll
+    for (int rr = 0; rr < RPW; ++rr) {
+      const int row = wave * RPW + rr;
+      const int m = m0 + row;
+      if (m < p.d_ff && ncol_ok) {
+        float o[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) o[c] = lv[rr].get(c) + eta * out[row * kSTN + lane * 4 + c];
+        store_n<4>(shadow + size_t(m) * p.d_model + ncol, o);
+      }
+    }
+#pragma unroll
+    for (int rr = 0; rr < RPW; ++rr) lv[rr] = nx[rr];
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
 // WRITE, fp32 evidence: VALU rank-C update (fp32 products keep the small
 // tiny-config tolerance; bf16 operands would round Z and G)
 // ---------------------------------------------------------------------------
@@ -453,7 +612,14 @@ hipError_t launch_write_t(const WriteLaunch& L, hipStream_t stream) {
     p.z[b] = in ? L.z[b] : nullptr;
     p.g[b] = in ? L.g[b] : nullptr;
   }
-  if (L.io_bf16) {
+  if (L.io_bf16 && L.chunk <= kSMaxC) {
+    p.mt = (L.d_ff + kSTM - 1) / kSTM;
+    p.ntl = (L.d_model + kSTN - 1) / kSTN;
+    const int items = L.count * p.mt;
+    const int per_tile = std::max(1, std::min(items, kSBlocksTarget / p.ntl));
+    hipLaunchKernelGGL((write_stream_kernel<ST>), dim3(unsigned(per_tile * p.ntl)), dim3(256), 0,
+                       stream, p);
+  } else if (L.io_bf16) {
     const unsigned blocks = unsigned(L.count) * unsigned(p.mt) * unsigned(p.ntl);
     hipLaunchKernelGGL((write_mfma_kernel<ST>), dim3(blocks), dim3(256), 0, stream, p);
   } else {
