@@ -69,21 +69,28 @@ def measured_traffic(records):
 class LaunchTimer:
     """HIP events around every launch, on torch's current stream."""
 
-    def __init__(self, torch):
+    def __init__(self, torch, streams=()):
         self.torch = torch
         self.records = []
         self._open = None
+        self._streams = {s.cuda_stream: s for s in streams}
 
-    def begin(self, kind, count, chunk):
+    def begin(self, kind, count, chunk, stream):
+        st = self._stream(stream)
         e = self.torch.cuda.Event(enable_timing=True)
-        e.record()
-        self._open = (kind, count, chunk, e)
+        e.record(st)
+        self._open = (kind, count, chunk, e, st)
 
     def end(self):
+        kind, count, chunk, s, st = self._open
         e = self.torch.cuda.Event(enable_timing=True)
-        e.record()
-        kind, count, chunk, s = self._open
+        e.record(st)
         self.records.append((kind, count, chunk, s, e))
+
+    def _stream(self, handle):
+        if handle in self._streams:
+            return self._streams[handle]
+        return self.torch.cuda.current_stream()
 
     def summary(self, wl):
         K, N = wl.d_ff, wl.d_model
@@ -163,8 +170,13 @@ def run_gpu(args, wl, layers):
     keep = set(args.cpu_layers) if args.cpu_baseline == "on" else set()
     sess, X, Y, ZG, kept = prepare(wl, layers, n, args.threads, keep)
     log(f"setup {time.time() - t0:.1f} s")
-    stream = torch.cuda.current_stream()
-    sp = stream.cuda_stream
+    from paper_2605_28053_amd.serving import StreamPair
+    if args.streams == 2:
+        pair = StreamPair()
+        pair.wait_for_current()
+        sp, tstreams = pair, (pair.read_stream, pair.write_stream)
+    else:
+        sp, tstreams = torch.cuda.current_stream().cuda_stream, ()
     y_ptrs = [Y[i].data_ptr() for i in range(len(layers))]
 
     def one(t, timer=None):
@@ -177,7 +189,7 @@ def run_gpu(args, wl, layers):
     for t in range(args.warmup):
         one(t)
     torch.cuda.synchronize()
-    timer = LaunchTimer(torch) if args.kernel_events == "on" else None
+    timer = LaunchTimer(torch, tstreams) if args.kernel_events == "on" else None
     tokens = 0
     writes = 0
     torch.cuda.synchronize()
@@ -238,6 +250,8 @@ def main():
     ap.add_argument("--cpu-steps", type=int, default=30)
     ap.add_argument("--cpu-layers", type=int, nargs="+", default=[0, 1])
     ap.add_argument("--kernel-events", choices=["on", "off"], default="on")
+    ap.add_argument("--streams", type=int, choices=[1, 2], default=1,
+                    help="2: READ and WRITE groups on two streams, joined every step")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run 5 plain device copies of BYTES each (HBM counter calibration)")
     args = ap.parse_args()
@@ -290,6 +304,7 @@ def main():
             "io": wl.io_dtype, "state": wl.state_dtype, "accumulate": "f32",
             "write_chunk": wl.chunk, "tokens_timed": g["tokens"], "writes_timed": g["writes"],
             "parallelism": "single-gpu",
+            "streams": args.streams,
         },
     }
     if "read" in kern:

@@ -95,7 +95,7 @@ typedef struct rwttt_config {
     uint32_t d_model;           /* columns; multiple of 8                         */
     int32_t  io_dtype;          /* RWTTT_F32 / RWTTT_BF16: x, W0, y, Z, G         */
     int32_t  state_dtype;       /* RWTTT_F32 / RWTTT_BF16: fast-weight slots      */
-    uint32_t max_group;         /* largest READ group, 1..RWTTT_MAX_GROUP         */
+    uint32_t max_group;         /* largest group a call accepts, 1..RWTTT_MAX_GROUP */
     uint32_t reserved;          /* must be 0                                      */
     const void* const* w0;      /* [n_layers] device pointers to W0_l             */
     void* const* slots;         /* [n_owners*n_layers*2] device pointers; entry
@@ -108,9 +108,9 @@ typedef struct rwttt_config {
 } rwttt_config;
 
 /* Bytes of device workspace a context with this config needs: the READ
- * split-K partial sums, max_group x ceil(d_ff/256) x d_model fp32 values
- * (d_model rounded up to the column tile).  Only the shape fields and
- * max_group are read.  The workspace needs no initialisation. */
+ * split-K partial sums, n_owners x ceil(d_ff/256) x d_model fp32 values
+ * (d_model rounded up to the column tile), one region per owner.  Only the
+ * shape fields are read.  The workspace needs no initialisation. */
 rwttt_status rwttt_workspace_bytes(const rwttt_config* cfg, size_t* bytes);
 
 /* Create a context: copies the pointer tables, sets V(r) = 0, slot 0 live and
@@ -156,9 +156,11 @@ rwttt_status rwttt_plan(const rwttt_ctx* ctx, const rwttt_event* ev, uint32_t n_
  * ReturnOutputs).  y must not overlap x, W0 or any slot.  Results for an owner
  * are bit-identical whatever the group's size, order or other members.
  * An empty group returns RWTTT_OK and launches nothing.  Launches two kernels
- * on `stream` (split-K partial sums into the workspace, then their reduction);
- * the workspace is shared by all reads of a context, so reads of one context
- * must be ordered on the device (one stream, or event waits). */
+ * on `stream` (split-K partial sums into the owners' workspace regions, then
+ * their reduction).  Reads and writes of one context may run concurrently on
+ * different streams when they name disjoint owners (the serving contract
+ * gives each owner one transition per step); calls that share an owner must
+ * be ordered on the device (same stream, or an event wait). */
 rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
                         uint32_t layer, const void* x, void* y, void* stream);
 

@@ -82,7 +82,7 @@ rwttt_status rwttt_workspace_bytes(const rwttt_config* cfg, size_t* bytes) {
   if (s != RWTTT_OK) return s;
   if (!bytes) return RWTTT_E_INVALID;
   *bytes = rwttt::read_geometry(int(cfg->d_ff), int(cfg->d_model), cfg->state_dtype == RWTTT_BF16,
-                                int(cfg->max_group))
+                                int(cfg->n_owners))
                .total_bytes;
   return RWTTT_OK;
 }
@@ -100,7 +100,7 @@ rwttt_status rwttt_create(const rwttt_config* cfg, rwttt_ctx** out) {
   std::sort(sorted.begin(), sorted.end());
   if (std::adjacent_find(sorted.begin(), sorted.end()) != sorted.end()) return RWTTT_E_OWNER_ALIAS;
   const rwttt::ReadGeometry geo = rwttt::read_geometry(
-      int(cfg->d_ff), int(cfg->d_model), cfg->state_dtype == RWTTT_BF16, int(cfg->max_group));
+      int(cfg->d_ff), int(cfg->d_model), cfg->state_dtype == RWTTT_BF16, int(cfg->n_owners));
   if (cfg->workspace) {
     if ((reinterpret_cast<uintptr_t>(cfg->workspace) & 255u) != 0) return RWTTT_E_INVALID;
     if (cfg->workspace_bytes < geo.total_bytes) return RWTTT_E_CAPACITY;
@@ -262,7 +262,7 @@ rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t
   L.d_ff = int(ctx->cfg.d_ff);
   L.d_model = int(ctx->cfg.d_model);
   L.count = int(n);
-  L.max_group = int(ctx->cfg.max_group);
+  L.n_owners = int(ctx->cfg.n_owners);
   L.x = x;
   L.y = y;
   L.w0 = ctx->w0[layer];
@@ -285,7 +285,7 @@ rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_
   if (n == 0) return RWTTT_OK;
   if (!owner_map || !z || !g || layer >= ctx->cfg.n_layers || chunk == 0) return RWTTT_E_INVALID;
   if (chunk > (1u << 20)) return RWTTT_E_INVALID;
-  if (n > RWTTT_MAX_GROUP) return RWTTT_E_CAPACITY;
+  if (n > ctx->cfg.max_group) return RWTTT_E_CAPACITY;
   const uint32_t* owners = owner_map + group->first;
   rwttt_status why = RWTTT_OK;
   if (!ctx->distinct_owners(owners, n, &why)) return why;

@@ -23,15 +23,15 @@ struct ReadGeometry {
   int ks;       // K chunks
   int nt;       // column tiles
   int npad;     // nt * tile_n
-  size_t part_floats;    // partial sums: max_group * ks * npad
+  size_t part_floats;    // partial sums: n_owners * ks * npad
   size_t total_bytes;    // workspace bytes, 256-B aligned
 };
 
-ReadGeometry read_geometry(int d_ff, int d_model, int state_bf16, int max_group);
+ReadGeometry read_geometry(int d_ff, int d_model, int state_bf16, int n_owners);
 
 struct ReadLaunch {
   int io_bf16, state_bf16;
-  int d_ff, d_model, count, max_group;
+  int d_ff, d_model, count, n_owners;
   const void* x;             // [n_owners, d_ff], owner-indexed
   void* y;                   // [n_owners, d_model], owner-indexed
   const void* w0;            // [d_ff, d_model]

@@ -93,8 +93,11 @@ template <int N> __device__ __forceinline__ void store_n(uint16_t* p, const floa
 //    (dispatch is round-robin over the 8 XCDs by block index) so that W0 comes
 //    from HBM once and is re-read from that XCD's L2.  dW is streamed with
 //    non-temporal loads so it does not evict W0.  The four waves' sums are
-//    added through LDS in a fixed order into one partial per (slot, chunk).
+//    added through LDS in a fixed order into one partial per (owner, chunk).
 // 2. read_reduce_kernel: y[b, n] = sum over chunks, in chunk order.
+//
+// Partials are indexed by owner id, so concurrent reads of disjoint owner sets
+// (one per stream) never touch the same workspace bytes.
 //
 // Every order depends only on the matrix shape, so an owner's y is
 // bit-identical whatever the group's size, order or other members.
@@ -212,7 +215,7 @@ __global__ void __launch_bounds__(kReadThreads) read_partial_kernel(const ReadPa
 #pragma unroll
   for (int c = 0; c < COLS; ++c) red[wave][lane * COLS + c] = acc[c];
   __syncthreads();
-  float* dst = p.part + (size_t(b) * p.ks + kc) * p.npad + nt * TILE_N;
+  float* dst = p.part + (size_t(p.row[b]) * p.ks + kc) * p.npad + nt * TILE_N;
   for (int j = tid; j < TILE_N; j += kReadThreads)
     dst[j] = ((red[0][j] + red[1][j]) + red[2][j]) + red[3][j];
 }
@@ -222,7 +225,7 @@ __global__ void __launch_bounds__(256) read_reduce_kernel(const ReadParams p) {
   const int b = blockIdx.y;
   const int n = blockIdx.x * 256 + threadIdx.x;
   if (n >= p.d_model) return;
-  const float* q = p.part + size_t(b) * p.ks * p.npad + n;
+  const float* q = p.part + size_t(p.row[b]) * p.ks * p.npad + n;
   float s = 0.f;
   int k = 0;
   for (; k + 8 <= p.ks; k += 8) {
@@ -570,7 +573,7 @@ __global__ void __launch_bounds__(256) write_valu_kernel(const WriteParams p) {
 
 template <typename IO, typename ST>
 hipError_t launch_read_t(const ReadLaunch& L, hipStream_t stream) {
-  const ReadGeometry g = read_geometry(L.d_ff, L.d_model, L.state_bf16, L.max_group);
+  const ReadGeometry g = read_geometry(L.d_ff, L.d_model, L.state_bf16, L.n_owners);
   ReadParams p;
   p.x = L.x;
   p.y = L.y;
@@ -632,13 +635,13 @@ hipError_t launch_write_t(const WriteLaunch& L, hipStream_t stream) {
 
 }  // namespace
 
-ReadGeometry read_geometry(int d_ff, int d_model, int state_bf16, int max_group) {
+ReadGeometry read_geometry(int d_ff, int d_model, int state_bf16, int n_owners) {
   ReadGeometry g;
   const int tile = read_tile_n(state_bf16);
   g.ks = (d_ff + kReadChunk - 1) / kReadChunk;
   g.nt = (d_model + tile - 1) / tile;
   g.npad = g.nt * tile;
-  g.part_floats = size_t(max_group) * g.ks * g.npad;
+  g.part_floats = size_t(n_owners) * g.ks * g.npad;
   g.total_bytes = (g.part_floats * sizeof(float) + 255) / 256 * 256;
   return g;
 }

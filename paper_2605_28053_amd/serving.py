@@ -42,6 +42,35 @@ def to_host(t, dtype):
     return t.detach().float().cpu().numpy()
 
 
+class StreamPair:
+    """Two torch streams (default priority) for READ and WRITE groups.
+
+    join() makes each stream wait for the other's work so far: the next
+    step's reads see this step's committed candidates, and the next step's
+    WRITEs overwrite a shadow slot only after the reads that used it.
+    """
+
+    def __init__(self, device="cuda"):
+        self.read_stream = torch.cuda.Stream(device=device)
+        self.write_stream = torch.cuda.Stream(device=device)
+        self.read = self.read_stream.cuda_stream
+        self.write = self.write_stream.cuda_stream
+
+    def join(self):
+        e_r = torch.cuda.Event()
+        e_w = torch.cuda.Event()
+        e_r.record(self.read_stream)
+        e_w.record(self.write_stream)
+        self.read_stream.wait_event(e_w)
+        self.write_stream.wait_event(e_r)
+
+    def wait_for_current(self):
+        """Order both streams after the work already on torch's current stream."""
+        cur = torch.cuda.current_stream()
+        self.read_stream.wait_stream(cur)
+        self.write_stream.wait_stream(cur)
+
+
 @dataclass
 class StepResult:
     plan: R.PlanResult
@@ -129,9 +158,17 @@ class Session:
         x_ptrs[i], y_ptrs[i]: device addresses of [n_owners, d_ff] inputs and
         [n_owners, d_model] outputs of local layer i.  zg_ptrs[r] =
         (z_ptrs_per_layer, g_ptrs_per_layer) for each WRITE owner r.
-        ``timer``, if given, has begin(kind, count, chunk) / end() called
-        around every launch (kind "read" or "write") on the same stream.
+
+        ``stream`` is one HIP stream handle for every launch, or a
+        ``StreamPair``: READ groups then go on its read stream and WRITE groups
+        (token read and update) on its write stream, so groups of disjoint
+        owners overlap on the device; the pair is joined both ways at the end
+        of the step.  ``timer``, if given, has begin(kind, count, chunk,
+        stream) / end() called around every launch.
         """
+        pair = stream if isinstance(stream, StreamPair) else None
+        s_read = pair.read if pair else stream
+        s_write = pair.write if pair else stream
         wl = self.wl
         by_owner = {it.owner: it for it in items}
         plan = R.rwttt_plan(self.ctx, self.events(t, items), t)
@@ -145,11 +182,12 @@ class Session:
             emit = any(by_owner[r].emit for r in owners)
             is_write = g.effect == WRITE
             chunk = by_owner[owners[0]].chunk if is_write else 0
+            stream = s_write if is_write else s_read
             failed = False
             for i in range(self.L):
                 if emit:
                     if timer is not None:
-                        timer.begin("read", g.count, 0)
+                        timer.begin("read", g.count, 0, stream)
                     st = R.rwttt_read(self.ctx, g, plan.owner_map_c, i, x_ptrs[i], y_ptrs[i], stream)
                     if timer is not None:
                         timer.end()
@@ -159,7 +197,7 @@ class Session:
                     zs = [zg_ptrs[r][0][i] for r in owners]
                     gs = [zg_ptrs[r][1][i] for r in owners]
                     if timer is not None:
-                        timer.begin("write", g.count, chunk)
+                        timer.begin("write", g.count, chunk, stream)
                     st = R.rwttt_write(self.ctx, g, plan.owner_map_c, i, chunk, zs, gs, wl.eta, stream)
                     if timer is not None:
                         timer.end()
@@ -168,6 +206,8 @@ class Session:
                         failed = True
             if is_write:
                 write_groups.append((owners, failed))
+        if pair is not None:
+            pair.join()
         committed, rolled = [], []
         for owners, failed in write_groups:
             # the failure branch of Algorithm 1 rolls a failed group back;

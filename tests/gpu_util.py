@@ -55,7 +55,7 @@ def host_f64(t, dtype):
     return O.widen(to_host(t, dtype), dtype)
 
 
-def run_gpu_trace(wl, trace, src, steps, layers=None, cols=None, fail_hook=None):
+def run_gpu_trace(wl, trace, src, steps, layers=None, cols=None, fail_hook=None, stream=None):
     """Run steps of a trace through Session.step (the serving loop) and collect
     (StepResult, versions after the step, {(owner, layer): y row}) per step."""
     layers = list(range(wl.n_layers)) if layers is None else list(layers)
@@ -76,8 +76,11 @@ def run_gpu_trace(wl, trace, src, steps, layers=None, cols=None, fail_hook=None)
                     gd.append(to_device(G, wl.io_dtype))
                 keep += zd + gd
                 zg[it.owner] = ([z.data_ptr() for z in zd], [g.data_ptr() for g in gd])
+        if stream is not None:
+            stream.wait_for_current()
         res = sess.step(t, items, [x.data_ptr() for x in X], [y.data_ptr() for y in Y], zg,
-                        torch.cuda.current_stream().cuda_stream, fail_hook)
+                        torch.cuda.current_stream().cuda_stream if stream is None else stream,
+                        fail_hook)
         torch.cuda.synchronize()
         ys = {}
         for it in items:

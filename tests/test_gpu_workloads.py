@@ -86,3 +86,23 @@ def test_prefill8b_bf16_state_sampled():
     n_writes, n_fail, table = check_trace(wl, range(12), layers=[0])
     assert n_writes == 64 and n_fail == 0
     assert table.V == [8] * 8
+
+
+def test_two_stream_serving_is_bit_identical_to_one_stream():
+    """READ and WRITE groups on two joined streams give the same bits as one stream."""
+    from paper_2605_28053_amd.serving import StreamPair
+    wl = workload(3)
+    src = TensorSource(wl, memo=True)
+    src.prefetch(range(wl.n_owners), [0], 16)
+    trace = build_trace(wl, 12)
+    one, out1 = run_gpu_trace(wl, trace, src, range(12))
+    pair = StreamPair()
+    pair.wait_for_current()
+    two, out2 = run_gpu_trace(wl, trace, src, range(12), stream=pair)
+    for (r1, v1, y1), (r2, v2, y2) in zip(out1, out2):
+        assert plan_tuples(r1) == plan_tuples(r2) and v1 == v2
+        assert set(y1) == set(y2)
+        for k in y1:
+            assert np.array_equal(y1[k], y2[k]), k
+    for r in range(wl.n_owners):
+        assert torch.equal(one.live(r, 0), two.live(r, 0)), r
