@@ -22,12 +22,16 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// fp32 -> bf16 bits, round to nearest even; NaN stays a quiet NaN.
-__device__ __forceinline__ uint32_t bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 values -> packed bf16 pair (first in the low half), round to
+// nearest even: one v_cvt_pk_bf16_f32 on gfx950.
+__device__ __forceinline__ uint32_t bf16x2_rne(float lo, float hi) {
+  const bf16x2_t h = __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t);
+  return *reinterpret_cast<const uint32_t*>(&h);
 }
+__device__ __forceinline__ uint32_t bf16_rne(float f) { return bf16x2_rne(f, 0.f) & 0xffffu; }
 
 template <typename T> struct Elem;
 template <> struct Elem<float> {
@@ -71,8 +75,8 @@ template <int N> __device__ __forceinline__ void store_n(float* p, const float (
 template <int N> __device__ __forceinline__ void store_n(uint16_t* p, const float (&v)[N]) {
   static_assert(N == 4, "bf16 stores are 4 wide");
   uint2 t;
-  t.x = bf16_rne(v[0]) | (bf16_rne(v[1]) << 16);
-  t.y = bf16_rne(v[2]) | (bf16_rne(v[3]) << 16);
+  t.x = bf16x2_rne(v[0], v[1]);
+  t.y = bf16x2_rne(v[2], v[3]);
   *reinterpret_cast<uint2*>(p) = t;
 }
 
@@ -537,6 +541,208 @@ __global__ void __launch_bounds__(256) write_stream_kernel(const WriteParams p) 
 }
 
 // ---------------------------------------------------------------------------
+// WRITE, bf16 evidence, large chunk (C > 64): tiled GEMM
+// ---------------------------------------------------------------------------
+//
+// At C = 512 the update does 2C flop per state element and is near the MFMA
+// ridge, so it is organised as a GEMM.  Block tile 256 rows (d_ff) x 256
+// columns (d_model), eight waves of 64 x 128 (2 x 4 MFMA 32x32x16 blocks,
+// 128 accumulators per lane).  Ranks are consumed in chunks of 64.  Z and G
+// arrive rank-major, so each thread loads an 8 x 8 block of 16-bit values
+// (8 ranks x 8 columns) with 16-byte loads and transposes it in registers
+// (v_perm_b32) into 8 rank-contiguous rows.  LDS rows are 64 ranks (128 B)
+// with the eight 16-byte groups of row r stored in slot (group ^ (r & 7)):
+// the transposed stores and the MFMA operand reads are then free of bank
+// conflicts.  The next chunk's global loads are in flight while the MFMAs
+// consume the current one.  Each XCD keeps a fixed set of column tiles (so
+// its G tiles stay in its L2) and walks the (owner, row tile) list.  The
+// epilogue moves the accumulators through LDS in 64-row passes so that all
+// eight waves read live and write shadow as contiguous rows, converting to
+// bf16 with the hardware packed convert.
+
+constexpr int kGTM = 256;
+constexpr int kGTN = 256;
+constexpr int kGKC = 64;                                  // ranks per chunk = LDS row length
+constexpr int kGThreads = 512;                            // 8 waves: 4 in m x 2 in n, 64 x 128 each
+
+// Transpose an 8 x 8 block of 16-bit values: row k of the input is r[k] (8
+// values, two per word); output j holds column j as 8 values, two per word.
+__device__ __forceinline__ void transpose8x8(const uint4 (&r)[8], uint4 (&o)[8]) {
+  const uint32_t* w[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) w[k] = reinterpret_cast<const uint32_t*>(&r[k]);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    // even j: low halves of (row 2q, row 2q+1); odd j: high halves
+    const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+    o[j] = make_uint4(__builtin_amdgcn_perm(w[1][j >> 1], w[0][j >> 1], sel),
+                      __builtin_amdgcn_perm(w[3][j >> 1], w[2][j >> 1], sel),
+                      __builtin_amdgcn_perm(w[5][j >> 1], w[4][j >> 1], sel),
+                      __builtin_amdgcn_perm(w[7][j >> 1], w[6][j >> 1], sel));
+  }
+}
+
+// bf16 offset of 16-byte group g of LDS row r (rows of kGKC ranks, swizzled).
+__device__ __forceinline__ int gemm_lds_off(int r, int g) { return r * kGKC + ((g ^ (r & 7)) << 3); }
+
+// Loads one 8 x 8 block (8 ranks from c, 8 columns from col) of a rank-major
+// [chunk, ld] operand; zeros outside unless the block is known to be inside.
+__device__ __forceinline__ void gemm_load_block(const uint16_t* src, size_t ld, int c, int chunk,
+                                                int col, int lim, bool inside, uint4 (&st)[8]) {
+  const uint16_t* q = src + size_t(c) * ld + col;
+  if (inside) {
+#pragma unroll
+    for (int r = 0; r < 8; ++r) st[r] = *reinterpret_cast<const uint4*>(q + size_t(r) * ld);
+  } else {
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+      st[r] = (c + r < chunk && col < lim) ? *reinterpret_cast<const uint4*>(q + size_t(r) * ld)
+                                           : make_uint4(0, 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ void gemm_store_block(uint16_t* lds, int row0, int g, const uint4 (&st)[8]) {
+  uint4 o[8];
+  transpose8x8(st, o);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) *reinterpret_cast<uint4*>(&lds[gemm_lds_off(row0 + j, g)]) = o[j];
+}
+
+template <typename ST>
+__global__ void __launch_bounds__(kGThreads, 1) write_gemm_kernel(const WriteParams p) {
+  constexpr int SC = 4;                                                   // columns per lane
+  __shared__ __attribute__((aligned(16))) uint16_t lds[(kGTM + kGTN) * kGKC];   // 64 KB
+  float* out = reinterpret_cast<float*>(lds);                             // [64][kGTN] in the epilogue
+  uint16_t* A = lds;                                                      // [kGTM][kGKC]
+  uint16_t* B = lds + kGTM * kGKC;                                        // [kGTN][kGKC]
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int half = lane >> 5;
+  // block -> XCD -> (row item, column tile owned by that XCD)
+  const int xcd = blockIdx.x & 7;
+  const int pos = blockIdx.x >> 3;
+  const int ntl8 = (p.ntl + 7) / 8;
+  const int rowid = pos / ntl8;
+  const int nt = (pos - rowid * ntl8) * 8 + xcd;
+  if (nt >= p.ntl || rowid >= p.count * p.mt) return;
+  const int b = rowid / p.mt;
+  const int mt = rowid - b * p.mt;
+  const int m0 = mt * kGTM;
+  const int n0 = nt * kGTN;
+  const bool interior = m0 + kGTM <= p.d_ff && n0 + kGTN <= p.d_model;
+  const uint16_t* Z = static_cast<const uint16_t*>(p.z[b]);
+  const uint16_t* G = static_cast<const uint16_t*>(p.g[b]);
+  const int wm = wave & 3;
+  const int wn = wave >> 2;
+
+  // staging: threads 0..255 one 8x8 block of G, 256..511 one of Z; consecutive
+  // lanes take different rank groups, so the swizzled stores do not conflict
+  const int sg = tid & 7;
+  const bool is_b = tid < 256;
+  const int srow = ((tid & 255) >> 3) * 8;
+  const uint16_t* ssrc = is_b ? G : Z;
+  const size_t sld = size_t(is_b ? p.d_model : p.d_ff);
+  const int scol = (is_b ? n0 : m0) + srow;
+  const int slim = is_b ? p.d_model : p.d_ff;
+  uint16_t* sdst = is_b ? B : A;
+  uint4 st[8];
+
+  f32x16_t acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
+
+  // live rows of an epilogue pass (8 per wave), prefetched one step ahead
+  const ST* live = static_cast<const ST*>(p.live[b]);
+  ST* shadow = static_cast<ST*>(p.shadow[b]);
+  const int ncol = n0 + lane * SC;
+  const bool ncol_ok = ncol < p.d_model;
+  Packed<ST, SC> lv[8];
+  auto load_live = [&](int ps) {
+    const int mrow0 = m0 + ps * 64 + wave * 8;
+#pragma unroll
+    for (int rr = 0; rr < 8; ++rr) {
+      if (interior || (mrow0 + rr < p.d_ff && ncol_ok))
+        load_packed<true>(live + size_t(mrow0 + rr) * p.d_model + ncol, lv[rr]);
+      else
+        lv[rr].zero();
+    }
+  };
+
+  const int nchunks = (p.chunk + kGKC - 1) / kGKC;
+  gemm_load_block(ssrc, sld, sg * 8, p.chunk, scol, slim, interior && kGKC <= p.chunk, st);
+  for (int k = 0; k < nchunks; ++k) {
+    gemm_store_block(sdst, srow, sg, st);
+    __syncthreads();
+    if (k + 1 < nchunks)
+      gemm_load_block(ssrc, sld, (k + 1) * kGKC + sg * 8, p.chunk, scol, slim,
+                      interior && (k + 2) * kGKC <= p.chunk, st);
+#pragma unroll
+    for (int ks = 0; ks < kGKC / 16; ++ks) {
+      const int g = ks * 2 + half;
+      bf16x8_t af[2], bfr[4];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        af[i] = *reinterpret_cast<const bf16x8_t*>(&A[gemm_lds_off(wm * 64 + i * 32 + (lane & 31), g)]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        bfr[j] = *reinterpret_cast<const bf16x8_t*>(&B[gemm_lds_off(wn * 128 + j * 32 + (lane & 31), g)]);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+
+  // Epilogue: pass ps moves tile rows [64 ps, 64 ps + 64) -- the accumulators of the two waves
+  // with wm == ps -- through LDS; then every wave updates 8 whole rows.  Accumulator register
+  // 4q+e of lane l holds D[8q + 4(l/32) + e][l % 32] of its 32x32 block.  Row r of the LDS
+  // tile keeps its columns XOR 32 * ((r >> 2) & 1), so the two half-waves of one write (rows
+  // 4 apart) use different banks; a lane's four columns stay contiguous.
+  const float eta = p.eta;
+  load_live(0);
+#pragma unroll
+  for (int ps = 0; ps < kGTM / 64; ++ps) {
+    if (wm == ps) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+            out[row * kGTN + ((wn * 128 + j * 32 + (lane & 31)) ^ (half << 5))] = acc[i][j][r];
+          }
+    }
+    __syncthreads();
+    const int mrow0 = m0 + ps * 64 + wave * 8;
+    const int nrow0 = mrow0 + 64;
+#pragma unroll
+    for (int rr = 0; rr < 8; ++rr) {
+      const int lr = wave * 8 + rr;
+      const float4 a4 = *reinterpret_cast<const float4*>(&out[lr * kGTN + ((lane * SC) ^ (((lr >> 2) & 1) << 5))]);
+      const float o[SC] = {lv[rr].get(0) + eta * a4.x, lv[rr].get(1) + eta * a4.y,
+                           lv[rr].get(2) + eta * a4.z, lv[rr].get(3) + eta * a4.w};
+      if (interior || (mrow0 + rr < p.d_ff && ncol_ok))
+        store_n<SC>(shadow + size_t(mrow0 + rr) * p.d_model + ncol, o);
+      // this row's register slot now takes the same row of the next pass
+      if (ps + 1 < kGTM / 64) {
+        if (interior || (nrow0 + rr < p.d_ff && ncol_ok))
+          load_packed<true>(live + size_t(nrow0 + rr) * p.d_model + ncol, lv[rr]);
+        else
+          lv[rr].zero();
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
 // WRITE, fp32 evidence: VALU rank-C update (fp32 products keep the small
 // tiny-config tolerance; bf16 operands would round Z and G)
 // ---------------------------------------------------------------------------
@@ -623,8 +829,11 @@ hipError_t launch_write_t(const WriteLaunch& L, hipStream_t stream) {
     hipLaunchKernelGGL((write_stream_kernel<ST>), dim3(unsigned(per_tile * p.ntl)), dim3(256), 0,
                        stream, p);
   } else if (L.io_bf16) {
-    const unsigned blocks = unsigned(L.count) * unsigned(p.mt) * unsigned(p.ntl);
-    hipLaunchKernelGGL((write_mfma_kernel<ST>), dim3(blocks), dim3(256), 0, stream, p);
+    p.mt = (L.d_ff + kGTM - 1) / kGTM;
+    p.ntl = (L.d_model + kGTN - 1) / kGTN;
+    const unsigned ntl8 = unsigned((p.ntl + 7) / 8);
+    hipLaunchKernelGGL((write_gemm_kernel<ST>), dim3(unsigned(L.count * p.mt) * ntl8 * 8u),
+                       dim3(kGThreads), 0, stream, p);
   } else {
     const size_t per_owner = size_t(L.d_ff) * (L.d_model / 4);
     const unsigned bx = unsigned((per_owner + 255) / 256);

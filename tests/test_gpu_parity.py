@@ -227,3 +227,57 @@ def test_read8_full_shape_matches_oracle():
             ref = O.round_to(O.read_apply(O.widen(X[r], "bf16"), W0, D[r]), "bf16")
             err = O.max_rel_floor(host_f64(y[r], "bf16"), ref)
             assert err <= BF16_OUT_TOL, (t, r, err)
+
+
+# --------------------------------------------------------------------------
+# exact bf16 rounding (round to nearest even, ties included)
+# --------------------------------------------------------------------------
+
+def test_read_bf16_output_rounding_is_exact():
+    """y = e_0 W0 + e_0 dW with W0 = 0 is exactly dW[0] in fp32; its bf16 bits must be RNE."""
+    d_ff, d_model, n = 256, 512, 2
+    wl = small_workload(d_ff, d_model, "bf16", "f32", n)
+    sess = Session(wl, None)
+    rng = np.random.default_rng(11)
+    base = (O.bf16_bits(O.bf16_round(rng.standard_normal(d_model))).astype(np.uint32) << 16)
+    row = np.where(rng.random(d_model) < 0.5, base | 0x8000, base | rng.integers(0, 0x10000, d_model))
+    row = row.astype(np.uint32).view(np.float32)
+    for r in range(n):
+        sess.slots[r][0][0].zero_()
+        sess.slots[r][0][0][0] = torch.from_numpy(row * (r + 1)).cuda()
+    sess.w0[0].zero_()
+    x = np.zeros((n, d_ff), dtype=np.uint16)
+    x[:, 0] = 0x3F80
+    y = torch.zeros((n, d_model), dtype=torch.bfloat16, device="cuda")
+    read_group(sess, [0, 1], 0, to_device(x, "bf16"), y)
+    torch.cuda.synchronize()
+    for r in range(n):
+        want = O.bf16_bits(O.round_to((row * (r + 1)).astype(np.float64), "bf16"))
+        assert np.array_equal(to_host(y[r], "bf16"), want), r
+
+
+@pytest.mark.parametrize("chunk", [1, 128])
+def test_write_bf16_state_rounding_is_exact(chunk):
+    """live + 1.0 * Z^T G with one unit rank is an exact fp32 sum; the bf16 shadow must be RNE.
+
+    chunk 1 takes the streaming WRITE kernel, chunk 128 the GEMM kernel.
+    """
+    d_ff, d_model = 256, 512
+    wl = small_workload(d_ff, d_model, "bf16", "bf16", 1, eta=1.0)
+    src = TensorSource(wl)
+    sess = Session(wl, src)
+    L = draw((d_ff, d_model), 1.0, "bf16", 3, (1,))
+    to_device(L, "bf16", out=sess.slots[0][0][0])
+    Z = np.zeros((chunk, d_ff), dtype=np.uint16)
+    Z[chunk - 1, :] = 0x3F80                     # rank chunk-1 is all ones
+    G = draw((chunk, d_model), 1.0, "bf16", 3, (2,))
+    st = write_group(sess, [0], 0, chunk, [to_device(Z, "bf16")], [to_device(G, "bf16")], eta=1.0)
+    assert st == R.RWTTT_OK
+    torch.cuda.synchronize()
+    want = O.bf16_bits(O.round_to(O.write_candidate(O.widen(L, "bf16"), O.widen(Z, "bf16"),
+                                                    O.widen(G, "bf16"), 1.0), "bf16"))
+    got = to_host(sess.shadow(0, 0), "bf16")
+    ties = np.mean((O.widen(L, "bf16") + O.widen(G[chunk - 1], "bf16")[None, :]) !=
+                   O.bf16_round(O.widen(L, "bf16") + O.widen(G[chunk - 1], "bf16")[None, :]))
+    say("inexact sums (rounded):", ties)
+    assert np.array_equal(got, want)
