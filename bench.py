@@ -96,7 +96,7 @@ class LaunchTimer:
         K, N = wl.d_ff, wl.d_model
         io, st = wl.io_bytes, (4 if wl.state_dtype == "f32" else 2)
         out = {}
-        for kind in ("read", "write"):
+        for kind in ("read", "write", "write_token"):
             recs = [r for r in self.records if r[0] == kind]
             if not recs:
                 continue
@@ -105,8 +105,12 @@ class LaunchTimer:
                 byt = sum(K * N * (io + b * st) + b * io * (K + N) for _, b, _, _, _ in recs)
                 flop = sum(4.0 * b * K * N for _, b, _, _, _ in recs)
             else:
-                byt = sum(b * (2 * st * K * N + io * c * (K + N)) for _, b, c, _, _ in recs)
-                flop = sum(2.0 * b * c * K * N for _, b, c, _, _ in recs)
+                # live read + shadow write + Z, G; with the token also W0 once and x, y
+                tok = kind == "write_token"
+                byt = sum(b * (2 * st * K * N + io * c * (K + N))
+                          + (K * N * io + b * io * (K + N) if tok else 0) for _, b, c, _, _ in recs)
+                flop = sum(2.0 * b * c * K * N + (4.0 * b * K * N if tok else 0)
+                           for _, b, c, _, _ in recs)
             out[kind] = dict(launches=len(recs), total_ms=ms, avg_us=1e3 * ms / len(recs),
                              bytes=byt, flops=flop, records=recs,
                              gbs=byt / (ms * 1e-3) / 1e9, tflops=flop / (ms * 1e-3) / 1e12)
@@ -317,9 +321,12 @@ def main():
                             "algorithmic_bytes_per_launch": round(rd["bytes"] / rd["launches"]),
                             "avg_launch_us": round(rd["avg_us"], 2),
                             "launches": rd["launches"]}
-    if "write" in kern:
-        wr = kern["write"]
-        line["write_kernel"] = {"achieved_gbs": round(wr["gbs"], 1),
+    wkind = "write_token" if "write_token" in kern else "write"
+    if wkind in kern:
+        wr = kern[wkind]
+        line["write_kernel"] = {"kernel": ("write_stream_kernel+read_reduce_kernel (token fused)"
+                                           if wkind == "write_token" else "write update"),
+                                "achieved_gbs": round(wr["gbs"], 1),
                                 "hbm_frac": round(wr["gbs"] / HBM_PEAK_GBS, 4),
                                 "achieved_tflops": round(wr["tflops"], 2),
                                 "mfma_frac": round(wr["tflops"] / BF16_MFMA_PEAK_TFLOPS, 5),

@@ -109,8 +109,9 @@ typedef struct rwttt_config {
 
 /* Bytes of device workspace a context with this config needs: the READ
  * split-K partial sums, n_owners x ceil(d_ff/256) x d_model fp32 values
- * (d_model rounded up to the column tile), one region per owner.  Only the
- * shape fields are read.  The workspace needs no initialisation. */
+ * (d_model rounded up to the column tile), and the fused WRITE token's
+ * partial sums, n_owners x 48 x d_model fp32 values; one region per owner.
+ * Only the shape fields are read.  The workspace needs no initialisation. */
 rwttt_status rwttt_workspace_bytes(const rwttt_config* cfg, size_t* bytes);
 
 /* Create a context: copies the pointer tables, sets V(r) = 0, slot 0 live and
@@ -170,14 +171,27 @@ rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t
  * with Z_b = z[b] ([chunk, d_ff]) and G_b = g[b] ([chunk, d_model]); the
  * product accumulates in fp32 and the result is rounded once to the state
  * dtype.  `z` and `g` are host arrays of group.count device pointers.  The
- * group must have effect RWTTT_WRITE.  Marks each owner dirty (its write view
- * is open until commit or rollback, Section 4.1).  Errors: RWTTT_E_DIRTY if
- * this layer of an owner was already written in the open transition.  If the
- * launch fails (RWTTT_E_HIP) or a failure was injected (RWTTT_E_WRITE_FAILED),
- * the owners stay dirty and are marked failed: they can only roll back. */
+ * group must have effect RWTTT_WRITE.
+ *
+ * A WRITE transition also returns the step's output (Section 3: Write_theta
+ * maps (r, x_r, u_r, s_r^v) to (y_r, s_r^{v+1})): with x and y non-null
+ * (owner-indexed as in rwttt_read) it also computes
+ *     y[r, :] = x[r, :] W0_layer + x[r, :] live_{r,layer}
+ * at version v, the candidate being invisible until commit.  For bf16
+ * evidence and chunk <= 64 the token is fused into the update kernel, which
+ * reads the live state once for both; otherwise the library runs a READ of
+ * the group first.  Pass x = y = NULL for a WRITE without a token (prefill).
+ *
+ * Marks each owner dirty (its write view is open until commit or rollback,
+ * Section 4.1).  Errors: RWTTT_E_INVALID if only one of x, y is given;
+ * RWTTT_E_DIRTY if this layer of an owner was already written in the open
+ * transition.  If the launch fails (RWTTT_E_HIP) or a failure was injected
+ * (RWTTT_E_WRITE_FAILED), the owners stay dirty and are marked failed: they
+ * can only roll back. */
 rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
                          uint32_t layer, uint32_t chunk, const void* const* z,
-                         const void* const* g, float eta, void* stream);
+                         const void* const* g, float eta, const void* x, void* y,
+                         void* stream);
 
 /* Commit (Section 4.2 CONTROL; Algorithm 1, CommitVersions): for each owner,
  * flip the live slot of every layer written in its open transition and set

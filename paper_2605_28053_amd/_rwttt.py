@@ -72,7 +72,8 @@ def _load():
                              P(rwttt_group), U32, P(U32), P(U32), U32, P(U32),
                              P(U32), U32, P(U32), P(I32)]),
         "rwttt_read": (I32, [VP, P(rwttt_group), P(U32), U32, VP, VP, VP]),
-        "rwttt_write": (I32, [VP, P(rwttt_group), P(U32), U32, U32, P(VP), P(VP), C.c_float, VP]),
+        "rwttt_write": (I32, [VP, P(rwttt_group), P(U32), U32, U32, P(VP), P(VP), C.c_float,
+                              VP, VP, VP]),
         "rwttt_commit": (I32, [VP, P(U32), U32]),
         "rwttt_rollback": (I32, [VP, P(U32), U32]),
         "rwttt_version": (I32, [VP, U32, P(U64), P(I32)]),
@@ -185,12 +186,15 @@ def rwttt_read(ctx, group, owner_map, layer, x_ptr, y_ptr, stream=0):
                            int(stream) or None)
 
 
-def rwttt_write(ctx, group, owner_map, layer, chunk, z_ptrs, g_ptrs, eta, stream=0):
+def rwttt_write(ctx, group, owner_map, layer, chunk, z_ptrs, g_ptrs, eta, x_ptr=0, y_ptr=0,
+                stream=0):
+    """x_ptr/y_ptr: the WRITE step's owner-indexed token input/output (0: no token)."""
     n = len(z_ptrs)
     z = (C.c_void_p * max(1, n))(*[int(p) for p in z_ptrs])
     g = (C.c_void_p * max(1, n))(*[int(p) for p in g_ptrs])
     return _lib.rwttt_write(ctx, C.byref(group), owner_map, int(layer), int(chunk), z, g,
-                            float(eta), int(stream) or None)
+                            float(eta), int(x_ptr) or None, int(y_ptr) or None,
+                            int(stream) or None)
 
 
 def rwttt_commit(ctx, owners):

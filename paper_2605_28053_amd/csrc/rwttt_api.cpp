@@ -278,12 +278,14 @@ rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t
 
 rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
                          uint32_t layer, uint32_t chunk, const void* const* z, const void* const* g,
-                         float eta, void* stream) {
+                         float eta, const void* x, void* y, void* stream) {
   if (!ctx || !group) return RWTTT_E_INVALID;
   if (group->effect != RWTTT_WRITE) return RWTTT_E_KEY_MISMATCH;
   const uint32_t n = group->count;
   if (n == 0) return RWTTT_OK;
   if (!owner_map || !z || !g || layer >= ctx->cfg.n_layers || chunk == 0) return RWTTT_E_INVALID;
+  if ((x == nullptr) != (y == nullptr)) return RWTTT_E_INVALID;
+  if (x && (!ctx->cfg.workspace || !aligned16(x) || !aligned16(y))) return RWTTT_E_INVALID;
   if (chunk > (1u << 20)) return RWTTT_E_INVALID;
   if (n > ctx->cfg.max_group) return RWTTT_E_CAPACITY;
   const uint32_t* owners = owner_map + group->first;
@@ -315,12 +317,18 @@ rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_
   L.d_model = int(ctx->cfg.d_model);
   L.count = int(n);
   L.chunk = int(chunk);
+  L.n_owners = int(ctx->cfg.n_owners);
   L.eta = eta;
+  L.x = x;
+  L.y = y;
+  L.w0 = ctx->w0[layer];
+  L.workspace = ctx->cfg.workspace;
   for (uint32_t b = 0; b < n; ++b) {
     L.live[b] = ctx->slot(owners[b], layer, 0);
     L.shadow[b] = ctx->slot(owners[b], layer, 1);
     L.z[b] = z[b];
     L.g[b] = g[b];
+    L.row[b] = owners[b];
   }
   const hipError_t e = rwttt::launch_write(L, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) {

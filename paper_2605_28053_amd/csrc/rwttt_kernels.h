@@ -23,7 +23,11 @@ struct ReadGeometry {
   int ks;       // K chunks
   int nt;       // column tiles
   int npad;     // nt * tile_n
-  size_t part_floats;    // partial sums: n_owners * ks * npad
+  size_t part_floats;    // READ partial sums: n_owners * ks * npad
+  int tparts;            // fused WRITE token: row-tile partitions per owner
+  int tnpad;             // fused WRITE token: partial row pitch
+  size_t token_offset;   // byte offset of the token partials, 256-B aligned
+  size_t token_floats;   // n_owners * tparts * tnpad
   size_t total_bytes;    // workspace bytes, 256-B aligned
 };
 
@@ -42,12 +46,17 @@ struct ReadLaunch {
 
 struct WriteLaunch {
   int io_bf16, state_bf16;
-  int d_ff, d_model, count, chunk;
+  int d_ff, d_model, count, chunk, n_owners;
   float eta;
+  const void* x;             // token inputs [n_owners, d_ff], or null for no token
+  void* y;                   // token outputs [n_owners, d_model]
+  const void* w0;            // W0 of the layer (token only)
+  void* workspace;           // ReadGeometry layout (token only)
   const void* live[RWTTT_MAX_GROUP];
   void* shadow[RWTTT_MAX_GROUP];
   const void* z[RWTTT_MAX_GROUP];    // [chunk, d_ff]
   const void* g[RWTTT_MAX_GROUP];    // [chunk, d_model]
+  uint32_t row[RWTTT_MAX_GROUP];     // owner id of each group slot
 };
 
 hipError_t launch_read(const ReadLaunch& L, hipStream_t stream);

@@ -244,276 +244,178 @@ __global__ void __launch_bounds__(256) read_reduce_kernel(const ReadParams p) {
 }
 
 // ---------------------------------------------------------------------------
-// WRITE, bf16 evidence: MFMA rank-C update
+// WRITE: shadow = live + eta Z^T G
 // ---------------------------------------------------------------------------
-//
-// Block tile: 128 rows (d_ff, "m") x 64 columns (d_model, "n") of one owner's
-// slot.  The MFMA computes the transposed tile D[n][m] = sum_c G[c][n] Z[c][m]
-// (A = G^T, B = Z) so that each lane's four consecutive accumulator rows are
-// four consecutive columns of the row-major slot: the epilogue reads live and
-// writes shadow with one 16-byte access per four values, no LDS round trip.
-// Z and G chunks of 32 ranks are staged through LDS transposed to
-// rank-contiguous rows, which is the operand layout the MFMA reads (eight
-// consecutive ranks per lane).
 
 struct WriteParams {
   int count, chunk, d_ff, d_model, mt, ntl;
+  int parts, npadw;          // streaming path: row-tile partitions per owner; token partial pitch
   float eta;
+  const void* x;             // fused token: [n_owners, d_ff] owner-indexed inputs, or null
+  const void* w0;            // fused token: W0 of the layer
+  float* tpart;              // fused token: [n_owners][parts][npadw] partial sums
   const void* live[RWTTT_MAX_GROUP];
   void* shadow[RWTTT_MAX_GROUP];
   const void* z[RWTTT_MAX_GROUP];
   const void* g[RWTTT_MAX_GROUP];
+  uint32_t row[RWTTT_MAX_GROUP];   // owner id of each group slot
 };
-
-constexpr int kWTM = 128;
-constexpr int kWTN = 64;
-constexpr int kWKC = 32;
-constexpr int kWPitch = kWKC + 8;   // bf16 elements per LDS row (80 B, 16-B aligned)
-
-template <typename ST>
-__global__ void __launch_bounds__(256) write_mfma_kernel(const WriteParams p) {
-  constexpr int SC = 4;   // state columns per accumulator group
-  __shared__ __attribute__((aligned(16))) uint16_t zt[kWTM * kWPitch];
-  __shared__ __attribute__((aligned(16))) uint16_t gt[kWTN * kWPitch];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int tiles = p.mt * p.ntl;
-  const int b = blockIdx.x / tiles;
-  const int rem = blockIdx.x - b * tiles;
-  const int mt = rem / p.ntl;
-  const int ntile = rem - mt * p.ntl;
-  const int m0 = mt * kWTM;
-  const int n0 = ntile * kWTN;
-  const ST* live = static_cast<const ST*>(p.live[b]);
-  ST* shadow = static_cast<ST*>(p.shadow[b]);
-  const uint16_t* Z = static_cast<const uint16_t*>(p.z[b]);
-  const uint16_t* G = static_cast<const uint16_t*>(p.g[b]);
-
-  const int half = lane >> 5;
-  const int m = m0 + wave * 32 + (lane & 31);
-  const bool m_ok = m < p.d_ff;
-
-  // Issue the live-state loads first; they are the bulk of the traffic.
-  float lv[2][4][SC];
-#pragma unroll
-  for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int n = n0 + nb * 32 + q * 8 + half * 4;
-      if (m_ok && n < p.d_model) {
-        load_n<SC>(live + size_t(m) * p.d_model + n, lv[nb][q]);
-      } else {
-#pragma unroll
-        for (int i = 0; i < SC; ++i) lv[nb][q][i] = 0.f;
-      }
-    }
-
-  f32x16_t acc0 = {}, acc1 = {};
-  for (int c0 = 0; c0 < p.chunk; c0 += kWKC) {
-    {  // Z chunk [32 ranks][128 m] -> zt[m][rank]
-      const int cp = tid >> 4;
-      const int mg = tid & 15;
-      const int mm = m0 + mg * 8;
-      const int c = c0 + 2 * cp;
-      uint4 r0 = make_uint4(0, 0, 0, 0), r1 = make_uint4(0, 0, 0, 0);
-      if (mm < p.d_ff) {
-        if (c < p.chunk) r0 = *reinterpret_cast<const uint4*>(Z + size_t(c) * p.d_ff + mm);
-        if (c + 1 < p.chunk) r1 = *reinterpret_cast<const uint4*>(Z + size_t(c + 1) * p.d_ff + mm);
-      }
-      const uint32_t a[4] = {r0.x, r0.y, r0.z, r0.w};
-      const uint32_t bb[4] = {r1.x, r1.y, r1.z, r1.w};
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        *reinterpret_cast<uint32_t*>(&zt[(mg * 8 + 2 * j) * kWPitch + 2 * cp]) =
-            (a[j] & 0xffffu) | (bb[j] << 16);
-        *reinterpret_cast<uint32_t*>(&zt[(mg * 8 + 2 * j + 1) * kWPitch + 2 * cp]) =
-            (a[j] >> 16) | (bb[j] & 0xffff0000u);
-      }
-    }
-    if (tid < 128) {  // G chunk [32 ranks][64 n] -> gt[n][rank]
-      const int cp = tid >> 3;
-      const int ng = tid & 7;
-      const int nn = n0 + ng * 8;
-      const int c = c0 + 2 * cp;
-      uint4 r0 = make_uint4(0, 0, 0, 0), r1 = make_uint4(0, 0, 0, 0);
-      if (nn < p.d_model) {
-        if (c < p.chunk) r0 = *reinterpret_cast<const uint4*>(G + size_t(c) * p.d_model + nn);
-        if (c + 1 < p.chunk) r1 = *reinterpret_cast<const uint4*>(G + size_t(c + 1) * p.d_model + nn);
-      }
-      const uint32_t a[4] = {r0.x, r0.y, r0.z, r0.w};
-      const uint32_t bb[4] = {r1.x, r1.y, r1.z, r1.w};
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        *reinterpret_cast<uint32_t*>(&gt[(ng * 8 + 2 * j) * kWPitch + 2 * cp]) =
-            (a[j] & 0xffffu) | (bb[j] << 16);
-        *reinterpret_cast<uint32_t*>(&gt[(ng * 8 + 2 * j + 1) * kWPitch + 2 * cp]) =
-            (a[j] >> 16) | (bb[j] & 0xffff0000u);
-      }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int ks = 0; ks < kWKC; ks += 16) {
-      const int kk = ks + half * 8;
-      const bf16x8_t bz = *reinterpret_cast<const bf16x8_t*>(&zt[(wave * 32 + (lane & 31)) * kWPitch + kk]);
-      const bf16x8_t a0 = *reinterpret_cast<const bf16x8_t*>(&gt[(lane & 31) * kWPitch + kk]);
-      const bf16x8_t a1 = *reinterpret_cast<const bf16x8_t*>(&gt[(32 + (lane & 31)) * kWPitch + kk]);
-      acc0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, bz, acc0, 0, 0, 0);
-      acc1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, bz, acc1, 0, 0, 0);
-    }
-    __syncthreads();
-  }
-
-  // Accumulator register 4q+i of lane l holds D[8q + 4(l/32) + i][l % 32].
-  const float eta = p.eta;
-#pragma unroll
-  for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int n = n0 + nb * 32 + q * 8 + half * 4;
-      if (!(m_ok && n < p.d_model)) continue;
-      float out[SC];
-#pragma unroll
-      for (int i = 0; i < SC; ++i) {
-        const float a = nb == 0 ? acc0[4 * q + i] : acc1[4 * q + i];
-        out[i] = lv[nb][q][i] + eta * a;
-      }
-      store_n<SC>(shadow + size_t(m) * p.d_model + n, out);
-    }
-}
 
 // ---------------------------------------------------------------------------
 // WRITE, bf16 evidence, small chunk (C <= 64): streaming rank-C update
 // ---------------------------------------------------------------------------
 //
 // For C <= 64 the update moves 2 x |dW| bytes for only 2C flop per element,
-// so it is HBM-bound and must stream like a copy.  A persistent grid of blocks
-// each keeps one 256-column tile of d_model and walks (owner, 32-row tile)
-// items.  Per owner, each wave loads its two 32-column blocks of G once into
-// MFMA operand registers.  Per item: Z's 32 x C tile is staged through LDS
-// transposed to rank-contiguous rows, eight or fewer MFMAs form
+// so it is HBM-bound and must stream like a copy: what matters is how many
+// bytes each CU keeps in flight.  Each block owns one (group slot, 256-column
+// tile, partition) and walks the partition's 32-row items (row tiles part,
+// part + P, part + 2P, ...; P fixed by the shape).  The owner's G tile is
+// staged once per block into LDS, transposed to rank-contiguous rows.  Per
+// item, everything the next item needs from HBM (its live rows, its Z tile,
+// and for the token its W0 rows and x values) is requested first; then Z's
+// 32 x C tile goes through LDS to rank-contiguous rows, the MFMAs form
 // D[m][n] = sum_c Z[c][m] G[c][n], the accumulators go through LDS, and every
-// wave reads, updates and stores whole 1 KB rows of the slot while the next
-// item's live rows are already loading.
+// wave reads, updates and stores whole 1 KB rows of the slot.  No load is on
+// the critical path of the item that issues it.
+//
+// With a fused token (the WRITE step's own output, read at version v before
+// the candidate is committed) the block also loads the same rows of W0 and
+// accumulates x[m] * live[m] + x[m] * W0[m] over its items: the live state is
+// read once for both the token and the update.  Per-(owner, partition)
+// partials are reduced in partition order by read_reduce_kernel.  The blocks
+// of all slots for one (tile, partition) sit on one XCD so that W0 comes from
+// HBM once.  The partition of an owner's rows never depends on the group, so
+// an owner's token and candidate are bit-identical in any group.
 
 constexpr int kSTM = 32;                 // rows per item
 constexpr int kSTN = 256;                // columns per tile
 constexpr int kSMaxC = 64;               // largest chunk on this path
-static_assert(kSMaxC * kSTN * 2 <= kSTM * kSTN * 4, "G tile must fit the output buffer");
-constexpr int kSPitch = kSMaxC + 8;      // bf16 per staged Z row (144 B, 16-B aligned)
-constexpr int kSBlocksTarget = 512;      // about two resident blocks per CU
+constexpr int kSPitch = kSMaxC + 8;      // bf16 per staged rank row (144 B: 16 rows hit 16 bank groups)
+constexpr int kSParts = 48;              // row-tile partitions per (owner, column tile)
 
-template <typename ST>
-__device__ __forceinline__ void stream_load_rows(const ST* live, int d_ff, int d_model, int m0,
+template <typename T>
+__device__ __forceinline__ void stream_load_rows(const T* base, int d_ff, int d_model, int m0,
                                                  int wave, int ncol, bool ncol_ok,
-                                                 Packed<ST, 4> (&lv)[kSTM / 4]) {
+                                                 Packed<T, 4> (&v)[kSTM / 4]) {
 #pragma unroll
   for (int rr = 0; rr < kSTM / 4; ++rr) {
     const int m = m0 + wave * (kSTM / 4) + rr;
-    if (m < d_ff && ncol_ok) load_packed<true>(live + size_t(m) * d_model + ncol, lv[rr]);
-    else lv[rr].zero();
+    if (m < d_ff && ncol_ok) load_packed<true>(base + size_t(m) * d_model + ncol, v[rr]);
+    else v[rr].zero();
   }
 }
 
-template <typename ST>
-__global__ void __launch_bounds__(256) write_stream_kernel(const WriteParams p) {
+// Ranks 2cp, 2cp+1 of eight consecutive rows starting at r0 of a rank-major
+// [C][ld] bf16 matrix (threads 0..127: cp = tid / 4, rows r0 + 8 (tid % 4)).
+__device__ __forceinline__ void stream_load_pair(const uint16_t* M, int ld, int rows, int chunk,
+                                                 int r0, int tid, uint4& a, uint4& b) {
+  a = make_uint4(0, 0, 0, 0);
+  b = make_uint4(0, 0, 0, 0);
+  const int cp = tid >> 2, r = r0 + (tid & 3) * 8, c = 2 * cp;
+  if (tid < 128 && r < rows) {
+    if (c < chunk) a = *reinterpret_cast<const uint4*>(M + size_t(c) * ld + r);
+    if (c + 1 < chunk) b = *reinterpret_cast<const uint4*>(M + size_t(c + 1) * ld + r);
+  }
+}
+
+// ...and their transpose into rank-contiguous LDS rows dst[row][rank].
+__device__ __forceinline__ void stream_store_pair(uint16_t* dst, int tid, int row0, uint4 a,
+                                                  uint4 b) {
+  if (tid >= 128) return;
+  const int cp = tid >> 2, r = row0 + (tid & 3) * 8;
+  const uint32_t x[4] = {a.x, a.y, a.z, a.w}, y[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    *reinterpret_cast<uint32_t*>(&dst[(r + 2 * q) * kSPitch + 2 * cp]) = (x[q] & 0xffffu) | (y[q] << 16);
+    *reinterpret_cast<uint32_t*>(&dst[(r + 2 * q + 1) * kSPitch + 2 * cp]) = (x[q] >> 16) | (y[q] & 0xffff0000u);
+  }
+}
+
+template <typename ST, bool TOKEN>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+write_stream_kernel(const WriteParams p) {
   constexpr int RPW = kSTM / 4;           // epilogue rows per wave
   constexpr int KSMAX = kSMaxC / 16;      // MFMA k-steps
   __shared__ __attribute__((aligned(16))) uint16_t zt[kSTM * kSPitch];
+  __shared__ __attribute__((aligned(16))) uint16_t gt[kSTN * kSPitch];
   __shared__ __attribute__((aligned(16))) float out[kSTM * kSTN];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int half = lane >> 5;
-  const int nt = blockIdx.x % p.ntl;
-  const int j0 = blockIdx.x / p.ntl;
-  const int jstep = gridDim.x / p.ntl;
-  const int items = p.count * p.mt;
-  if (j0 >= items) return;
+  // block -> (XCD, position) -> ((tile, partition) pair, slot)
+  const int xcd = blockIdx.x & 7;
+  const int pos = blockIdx.x >> 3;
+  const int pl = pos / p.count;
+  const int b = pos - pl * p.count;
+  const int pair = pl * 8 + xcd;
+  if (pair >= p.ntl * p.parts) return;
+  const int nt = pair / p.parts;
+  const int part = pair - nt * p.parts;   // parts <= mt: every partition has an item
   const int n0 = nt * kSTN;
   const int ncol = n0 + lane * 4;
   const bool ncol_ok = ncol < p.d_model;
   const int ksteps = (p.chunk + 15) / 16;
   const float eta = p.eta;
+  const ST* live = static_cast<const ST*>(p.live[b]);
+  ST* shadow = static_cast<ST*>(p.shadow[b]);
+  const uint16_t* Z = static_cast<const uint16_t*>(p.z[b]);
+  const uint16_t* G = static_cast<const uint16_t*>(p.g[b]);
+  const uint16_t* W0 = static_cast<const uint16_t*>(p.w0);
+  const uint16_t* X = static_cast<const uint16_t*>(p.x) + size_t(p.row[b]) * p.d_ff;
 
-  bf16x8_t gf[2][KSMAX];
-  int cur_b = -1;
-  Packed<ST, 4> lv[RPW];
-  {
-    const int b = j0 / p.mt;
-    stream_load_rows(static_cast<const ST*>(p.live[b]), p.d_ff, p.d_model, (j0 - b * p.mt) * kSTM,
-                     wave, ncol, ncol_ok, lv);
+  // G tile [C ranks][256 n] -> gt[n][rank], 32 columns per thread pass
+  for (int j = 0; j < kSTN / 32; ++j) {
+    uint4 ga, gb;
+    stream_load_pair(G, p.d_model, p.d_model, p.chunk, n0 + j * 32, tid, ga, gb);
+    stream_store_pair(gt, tid, j * 32, ga, gb);
   }
-  for (int j = j0; j < items; j += jstep) {
-    const int b = j / p.mt;
-    const int m0 = (j - b * p.mt) * kSTM;
-    const uint16_t* Z = static_cast<const uint16_t*>(p.z[b]);
-    if (b != cur_b) {
-      // Stage owner b's G tile [C ranks][256 n] through the idle output buffer,
-      // transposed to gs[n][rank] (64 ranks per row), and keep this wave's two
-      // 32-column blocks as MFMA operands for all of the owner's items.
-      const uint16_t* G = static_cast<const uint16_t*>(p.g[b]);
-      uint16_t* gs = reinterpret_cast<uint16_t*>(out);
-      for (int it = tid; it < (kSMaxC / 2) * (kSTN / 8); it += 256) {
-        const int cp = it >> 5, ng = it & 31;
-        const int nn = n0 + ng * 8, c = 2 * cp;
-        uint4 r0 = make_uint4(0, 0, 0, 0), r1 = make_uint4(0, 0, 0, 0);
-        if (nn < p.d_model) {
-          if (c < p.chunk) r0 = *reinterpret_cast<const uint4*>(G + size_t(c) * p.d_model + nn);
-          if (c + 1 < p.chunk) r1 = *reinterpret_cast<const uint4*>(G + size_t(c + 1) * p.d_model + nn);
-        }
-        const uint32_t a[4] = {r0.x, r0.y, r0.z, r0.w}, bb[4] = {r1.x, r1.y, r1.z, r1.w};
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          *reinterpret_cast<uint32_t*>(&gs[(ng * 8 + 2 * q) * kSMaxC + 2 * cp]) = (a[q] & 0xffffu) | (bb[q] << 16);
-          *reinterpret_cast<uint32_t*>(&gs[(ng * 8 + 2 * q + 1) * kSMaxC + 2 * cp]) = (a[q] >> 16) | (bb[q] & 0xffff0000u);
-        }
-      }
-      __syncthreads();
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int s = 0; s < KSMAX; ++s)
-          gf[i][s] = *reinterpret_cast<const bf16x8_t*>(
-              &gs[((wave * 2 + i) * 32 + (lane & 31)) * kSMaxC + s * 16 + half * 8]);
-      __syncthreads();
-      cur_b = b;
-    }
-    // Z tile [C ranks][32 m] -> zt[m][rank]; 128 threads, 2 ranks x 8 m each
-    if (tid < 128) {
-      const int cp = tid >> 2, mg = tid & 3;
-      const int mm = m0 + mg * 8, c = 2 * cp;
-      uint4 r0 = make_uint4(0, 0, 0, 0), r1 = make_uint4(0, 0, 0, 0);
-      if (mm < p.d_ff) {
-        if (c < p.chunk) r0 = *reinterpret_cast<const uint4*>(Z + size_t(c) * p.d_ff + mm);
-        if (c + 1 < p.chunk) r1 = *reinterpret_cast<const uint4*>(Z + size_t(c + 1) * p.d_ff + mm);
-      }
-      const uint32_t a[4] = {r0.x, r0.y, r0.z, r0.w}, bb[4] = {r1.x, r1.y, r1.z, r1.w};
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        *reinterpret_cast<uint32_t*>(&zt[(mg * 8 + 2 * q) * kSPitch + 2 * cp]) = (a[q] & 0xffffu) | (bb[q] << 16);
-        *reinterpret_cast<uint32_t*>(&zt[(mg * 8 + 2 * q + 1) * kSPitch + 2 * cp]) = (a[q] >> 16) | (bb[q] & 0xffff0000u);
-      }
-    }
+
+  // the first item's operands
+  float yacc[4] = {0.f, 0.f, 0.f, 0.f};
+  Packed<ST, 4> lv[RPW];
+  Packed<uint16_t, 4> wv[RPW];
+  uint4 za, zb, xq = make_uint4(0, 0, 0, 0);
+  stream_load_rows(live, p.d_ff, p.d_model, part * kSTM, wave, ncol, ncol_ok, lv);
+  stream_load_pair(Z, p.d_ff, p.d_ff, p.chunk, part * kSTM, tid, za, zb);
+  if (TOKEN) {
+    stream_load_rows(W0, p.d_ff, p.d_model, part * kSTM, wave, ncol, ncol_ok, wv);
+    if (part * kSTM + wave * RPW < p.d_ff)
+      xq = *reinterpret_cast<const uint4*>(X + part * kSTM + wave * RPW);
+  }
+
+  for (int mt = part; mt < p.mt; mt += p.parts) {
+    const int m0 = mt * kSTM;
+    const int mn = mt + p.parts;
+    stream_store_pair(zt, tid, 0, za, zb);
     __syncthreads();
+    // the next item's operands load while this one is computed and stored
+    Packed<ST, 4> nx[RPW];
+    Packed<uint16_t, 4> nw[RPW];
+    uint4 nxq = make_uint4(0, 0, 0, 0);
+    if (mn < p.mt) {
+      stream_load_rows(live, p.d_ff, p.d_model, mn * kSTM, wave, ncol, ncol_ok, nx);
+      stream_load_pair(Z, p.d_ff, p.d_ff, p.chunk, mn * kSTM, tid, za, zb);
+      if (TOKEN) {
+        stream_load_rows(W0, p.d_ff, p.d_model, mn * kSTM, wave, ncol, ncol_ok, nw);
+        if (mn * kSTM + wave * RPW < p.d_ff)
+          nxq = *reinterpret_cast<const uint4*>(X + mn * kSTM + wave * RPW);
+      }
+    }
     f32x16_t acc[2] = {f32x16_t{}, f32x16_t{}};
 #pragma unroll
     for (int s = 0; s < KSMAX; ++s) {
       if (s < ksteps) {
-        const bf16x8_t az = *reinterpret_cast<const bf16x8_t*>(&zt[(lane & 31) * kSPitch + s * 16 + half * 8]);
-        acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(az, gf[0][s], acc[0], 0, 0, 0);
-        acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(az, gf[1][s], acc[1], 0, 0, 0);
+        const int kofs = s * 16 + half * 8;
+        const bf16x8_t az = *reinterpret_cast<const bf16x8_t*>(&zt[(lane & 31) * kSPitch + kofs]);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const bf16x8_t bg = *reinterpret_cast<const bf16x8_t*>(
+              &gt[((wave * 2 + i) * 32 + (lane & 31)) * kSPitch + kofs]);
+          acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(az, bg, acc[i], 0, 0, 0);
+        }
       }
-    }
-    // the next item's live rows load while this one finishes
-    Packed<ST, 4> nx[RPW];
-    const int jn = j + jstep;
-    if (jn < items) {
-      const int bn = jn / p.mt;
-      stream_load_rows(static_cast<const ST*>(p.live[bn]), p.d_ff, p.d_model, (jn - bn * p.mt) * kSTM,
-                       wave, ncol, ncol_ok, nx);
     }
     // accumulator register 4q+e of lane l holds D[8q + 4(l/32) + e][l % 32]
 #pragma unroll
@@ -522,7 +424,6 @@ __global__ void __launch_bounds__(256) write_stream_kernel(const WriteParams p) 
       for (int r = 0; r < 16; ++r)
         out[(8 * (r >> 2) + 4 * half + (r & 3)) * kSTN + (wave * 2 + i) * 32 + (lane & 31)] = acc[i][r];
     __syncthreads();
-    ST* shadow = static_cast<ST*>(p.shadow[b]);
 #pragma unroll
     for (int rr = 0; rr < RPW; ++rr) {
       const int row = wave * RPW + rr;
@@ -534,9 +435,34 @@ __global__ void __launch_bounds__(256) write_stream_kernel(const WriteParams p) 
         store_n<4>(shadow + size_t(m) * p.d_model + ncol, o);
       }
     }
+    if (TOKEN) {
+      // token: x[m] * live[m] + x[m] * W0[m] over this wave's rows, in row order
+      const uint32_t xw[4] = {xq.x, xq.y, xq.z, xq.w};
 #pragma unroll
-    for (int rr = 0; rr < RPW; ++rr) lv[rr] = nx[rr];
+      for (int rr = 0; rr < RPW; ++rr) {
+        const float xv = (rr & 1) ? bf16_hi(xw[rr >> 1]) : bf16_lo(xw[rr >> 1]);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) yacc[c] = fmaf(xv, wv[rr].get(c), fmaf(xv, lv[rr].get(c), yacc[c]));
+      }
+    }
+    if (mn < p.mt) {
+#pragma unroll
+      for (int rr = 0; rr < RPW; ++rr) {
+        lv[rr] = nx[rr];
+        if (TOKEN) wv[rr] = nw[rr];
+      }
+      xq = nxq;
+    }
     __syncthreads();
+  }
+
+  if (TOKEN) {
+    // the four waves' token sums in wave order -> one partial per (owner, partition)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) out[wave * kSTN + lane * 4 + c] = yacc[c];
+    __syncthreads();
+    const float v = ((out[tid] + out[kSTN + tid]) + out[2 * kSTN + tid]) + out[3 * kSTN + tid];
+    p.tpart[(size_t(p.row[b]) * p.parts + part) * p.npadw + n0 + tid] = v;
   }
 }
 
@@ -812,23 +738,76 @@ hipError_t launch_write_t(const WriteLaunch& L, hipStream_t stream) {
   p.d_ff = L.d_ff;
   p.d_model = L.d_model;
   p.eta = L.eta;
-  p.mt = (L.d_ff + kWTM - 1) / kWTM;
-  p.ntl = (L.d_model + kWTN - 1) / kWTN;
+  p.parts = 0;
+  p.npadw = 0;
+  p.x = L.x;
+  p.w0 = L.w0;
+  p.tpart = nullptr;
   for (int b = 0; b < RWTTT_MAX_GROUP; ++b) {
     const bool in = b < L.count;
     p.live[b] = in ? L.live[b] : nullptr;
     p.shadow[b] = in ? L.shadow[b] : nullptr;
     p.z[b] = in ? L.z[b] : nullptr;
     p.g[b] = in ? L.g[b] : nullptr;
+    p.row[b] = in ? L.row[b] : 0u;
   }
+  const bool token = L.x != nullptr;
   if (L.io_bf16 && L.chunk <= kSMaxC) {
+    const ReadGeometry geo = read_geometry(L.d_ff, L.d_model, L.state_bf16, L.n_owners);
     p.mt = (L.d_ff + kSTM - 1) / kSTM;
     p.ntl = (L.d_model + kSTN - 1) / kSTN;
-    const int items = L.count * p.mt;
-    const int per_tile = std::max(1, std::min(items, kSBlocksTarget / p.ntl));
-    hipLaunchKernelGGL((write_stream_kernel<ST>), dim3(unsigned(per_tile * p.ntl)), dim3(256), 0,
-                       stream, p);
-  } else if (L.io_bf16) {
+    // partitions of an owner's row tiles: fixed by the shape, never by the group
+    p.parts = std::min(geo.tparts, p.mt);
+    p.npadw = geo.tnpad;
+    p.tpart = token ? reinterpret_cast<float*>(static_cast<char*>(L.workspace) + geo.token_offset) : nullptr;
+    const unsigned pairs8 = unsigned((p.ntl * p.parts + 7) / 8 * 8);
+    const dim3 grid(pairs8 * unsigned(L.count));
+    if (token) {
+      hipLaunchKernelGGL((write_stream_kernel<ST, true>), grid, dim3(256), 0, stream, p);
+      ReadParams q;
+      q.x = nullptr;
+      q.y = L.y;
+      q.w0 = nullptr;
+      q.part = p.tpart;
+      q.count = L.count;
+      q.d_ff = L.d_ff;
+      q.d_model = L.d_model;
+      q.ks = p.parts;
+      q.nt = p.ntl;
+      q.npad = p.npadw;
+      for (int b = 0; b < RWTTT_MAX_GROUP; ++b) {
+        q.dw[b] = nullptr;
+        q.row[b] = b < L.count ? L.row[b] : 0u;
+      }
+      hipLaunchKernelGGL((read_reduce_kernel<uint16_t>), dim3((L.d_model + 255) / 256, L.count),
+                         dim3(256), 0, stream, q);
+    } else {
+      hipLaunchKernelGGL((write_stream_kernel<ST, false>), grid, dim3(256), 0, stream, p);
+    }
+    return hipGetLastError();
+  }
+  if (token) {
+    // no fused kernel on this path: the token is an ordinary READ of the group at version v
+    ReadLaunch R;
+    R.io_bf16 = L.io_bf16;
+    R.state_bf16 = L.state_bf16;
+    R.d_ff = L.d_ff;
+    R.d_model = L.d_model;
+    R.count = L.count;
+    R.n_owners = L.n_owners;
+    R.x = L.x;
+    R.y = L.y;
+    R.w0 = L.w0;
+    R.workspace = L.workspace;
+    for (int b = 0; b < L.count; ++b) {
+      R.dw[b] = L.live[b];
+      R.row[b] = L.row[b];
+    }
+    const hipError_t e = L.io_bf16 ? launch_read_t<uint16_t, ST>(R, stream)
+                                   : launch_read_t<float, ST>(R, stream);
+    if (e != hipSuccess) return e;
+  }
+  if (L.io_bf16) {
     p.mt = (L.d_ff + kGTM - 1) / kGTM;
     p.ntl = (L.d_model + kGTN - 1) / kGTN;
     const unsigned ntl8 = unsigned((p.ntl + 7) / 8);
@@ -851,7 +830,12 @@ ReadGeometry read_geometry(int d_ff, int d_model, int state_bf16, int n_owners) 
   g.nt = (d_model + tile - 1) / tile;
   g.npad = g.nt * tile;
   g.part_floats = size_t(n_owners) * g.ks * g.npad;
-  g.total_bytes = (g.part_floats * sizeof(float) + 255) / 256 * 256;
+  // the fused WRITE token's partials follow, also one region per owner
+  g.tparts = kSParts;
+  g.tnpad = (d_model + kSTN - 1) / kSTN * kSTN;
+  g.token_offset = (g.part_floats * sizeof(float) + 255) / 256 * 256;
+  g.token_floats = size_t(n_owners) * g.tparts * g.tnpad;
+  g.total_bytes = g.token_offset + (g.token_floats * sizeof(float) + 255) / 256 * 256;
   return g;
 }
 

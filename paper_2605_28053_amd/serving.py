@@ -161,7 +161,7 @@ class Session:
 
         ``stream`` is one HIP stream handle for every launch, or a
         ``StreamPair``: READ groups then go on its read stream and WRITE groups
-        (token read and update) on its write stream, so groups of disjoint
+        (update with its token) on its write stream, so groups of disjoint
         owners overlap on the device; the pair is joined both ways at the end
         of the step.  ``timer``, if given, has begin(kind, count, chunk,
         stream) / end() called around every launch.
@@ -185,7 +185,26 @@ class Session:
             stream = s_write if is_write else s_read
             failed = False
             for i in range(self.L):
-                if emit:
+                need_token = emit
+                if is_write and not failed:
+                    # the WRITE transition returns the step's token with the candidate
+                    zs = [zg_ptrs[r][0][i] for r in owners]
+                    gs = [zg_ptrs[r][1][i] for r in owners]
+                    if timer is not None:
+                        timer.begin("write_token" if emit else "write", g.count, chunk, stream)
+                    st = R.rwttt_write(self.ctx, g, plan.owner_map_c, i, chunk, zs, gs, wl.eta,
+                                       x_ptrs[i] if emit else 0, y_ptrs[i] if emit else 0,
+                                       stream)
+                    if timer is not None:
+                        timer.end()
+                    statuses.append(st)
+                    if st == R.RWTTT_OK:
+                        need_token = False
+                    else:
+                        failed = True
+                if need_token:
+                    # READ groups, and the layers of a WRITE group whose update failed:
+                    # the token at the unchanged version v
                     if timer is not None:
                         timer.begin("read", g.count, 0, stream)
                     st = R.rwttt_read(self.ctx, g, plan.owner_map_c, i, x_ptrs[i], y_ptrs[i], stream)
@@ -193,17 +212,6 @@ class Session:
                         timer.end()
                     if st != R.RWTTT_OK:
                         raise R.RwtttError(st, "rwttt_read")
-                if is_write and not failed:
-                    zs = [zg_ptrs[r][0][i] for r in owners]
-                    gs = [zg_ptrs[r][1][i] for r in owners]
-                    if timer is not None:
-                        timer.begin("write", g.count, chunk, stream)
-                    st = R.rwttt_write(self.ctx, g, plan.owner_map_c, i, chunk, zs, gs, wl.eta, stream)
-                    if timer is not None:
-                        timer.end()
-                    statuses.append(st)
-                    if st != R.RWTTT_OK:
-                        failed = True
             if is_write:
                 write_groups.append((owners, failed))
         if pair is not None:

@@ -42,12 +42,15 @@ def read_group(sess, owners, li, x_dev, y_dev, effect=READ):
     assert st == R.RWTTT_OK, R.rwttt_strerror(st)
 
 
-def write_group(sess, owners, li, chunk, zs, gs, eta=None):
+def write_group(sess, owners, li, chunk, zs, gs, eta=None, x_dev=None, y_dev=None):
+    """One WRITE group; with x_dev/y_dev the step's token is returned in y_dev."""
     g = R.make_group(WRITE, 0, len(owners))
     st = R.rwttt_write(sess.ctx, g, R.u32_array(owners), li, chunk,
                        [z.data_ptr() for z in zs], [x.data_ptr() for x in gs],
                        sess.wl.eta if eta is None else eta,
-                       torch.cuda.current_stream().cuda_stream)
+                       0 if x_dev is None else x_dev.data_ptr(),
+                       0 if y_dev is None else y_dev.data_ptr(),
+                       stream=torch.cuda.current_stream().cuda_stream)
     return st
 
 

@@ -165,6 +165,90 @@ def test_write_commit_rollback_match_oracle(d_ff, d_model, io, state, chunk, gro
             assert slot_hash(sess.live(r, 0)) == shadow_hash[r]
 
 
+# --------------------------------------------------------------------------
+# WRITE with its token (the step's output at version v)
+# --------------------------------------------------------------------------
+
+TOKEN_CASES = [
+    # d_ff, d_model, io, state, chunk, group, n_owners
+    (40, 24, "bf16", "f32", 1, [2], 3),               # one row tile, one partition
+    (1000, 264, "bf16", "f32", 17, [0, 3, 1], 4),     # ragged rows and columns
+    (1000, 264, "bf16", "bf16", 64, [1, 2], 4),
+    (1576, 520, "bf16", "f32", 64, [4, 0, 2], 5),     # 50 row tiles over 48 partitions
+    (520, 1032, "bf16", "f32", 100, [3, 0], 4),       # large chunk: READ, then the GEMM
+    (256, 64, "f32", "f32", 4, [0, 1], 2),            # fp32 evidence
+    (9728, 2560, "bf16", "f32", 64, [5, 1, 7], 8),    # full 4B-layer shape
+]
+
+
+@pytest.mark.parametrize("d_ff,d_model,io,state,chunk,group,n_owners", TOKEN_CASES)
+def test_write_token_matches_oracle(d_ff, d_model, io, state, chunk, group, n_owners):
+    wl = small_workload(d_ff, d_model, io, state, n_owners, eta=0.05)
+    say("write+token", d_ff, d_model, io, state, chunk, group)
+    src = TensorSource(wl)
+    sess = Session(wl, src)
+    X = draw((n_owners, d_ff), 1.0, io, wl.seed, (77, 2))
+    xd = to_device(X, io)
+    tdt = torch.float32 if io == "f32" else torch.bfloat16
+    zs, gs = [], []
+    for r in group:
+        zs.append(to_device(draw((chunk, d_ff), 1.0, io, wl.seed, (78, r), absval=True), io))
+        gs.append(to_device(draw((chunk, d_model), 1.0, io, wl.seed, (79, r)), io))
+    sentinel = torch.full((n_owners, d_model), 7.0, dtype=tdt, device="cuda")
+    y = sentinel.clone()
+    st = write_group(sess, group, 0, chunk, zs, gs, x_dev=xd, y_dev=y)
+    assert st == R.RWTTT_OK, R.rwttt_strerror(st)
+    torch.cuda.synchronize()
+    W0 = O.widen(src.w0(0), io)
+    for r in group:
+        # the token reads version v: the candidate in the shadow slot is not visible
+        ref = O.round_to(O.read_apply(O.widen(X[r], io), W0, O.widen(src.dw_init(r, 0), state)), io)
+        assert O.max_rel_floor(host_f64(y[r], io), ref) <= out_tol(io), r
+    others = [r for r in range(n_owners) if r not in group]
+    if others:
+        assert torch.equal(y[others], sentinel[others])
+    shadow_tok = {r: slot_hash(sess.shadow(r, 0)) for r in group}
+    # the candidate does not depend on whether the token was asked for
+    assert R.rwttt_rollback(sess.ctx, group) == R.RWTTT_OK
+    assert write_group(sess, group, 0, chunk, zs, gs) == R.RWTTT_OK
+    torch.cuda.synchronize()
+    assert {r: slot_hash(sess.shadow(r, 0)) for r in group} == shadow_tok
+    # an owner's token is bit-identical alone and in any group order
+    assert R.rwttt_rollback(sess.ctx, group) == R.RWTTT_OK
+    y1 = sentinel.clone()
+    for i, r in enumerate(group):
+        assert write_group(sess, [r], 0, chunk, [zs[i]], [gs[i]], x_dev=xd, y_dev=y1) == R.RWTTT_OK
+        assert R.rwttt_rollback(sess.ctx, [r]) == R.RWTTT_OK
+    rev = list(reversed(range(len(group))))
+    y2 = sentinel.clone()
+    assert write_group(sess, [group[i] for i in rev], 0, chunk, [zs[i] for i in rev],
+                       [gs[i] for i in rev], x_dev=xd, y_dev=y2) == R.RWTTT_OK
+    torch.cuda.synchronize()
+    assert torch.equal(y[group], y1[group])
+    assert torch.equal(y[group], y2[group])
+    assert {r: slot_hash(sess.shadow(r, 0)) for r in group} == shadow_tok
+    # the token equals a READ of the same owners up to fp32 summation order
+    y3 = torch.zeros_like(y)
+    read_group(sess, group, 0, xd, y3)
+    torch.cuda.synchronize()
+    for r in group:
+        assert O.max_rel_floor(host_f64(y[r], io), host_f64(y3[r], io)) <= out_tol(io), r
+
+
+def test_write_token_argument_errors():
+    wl = small_workload(256, 64, "bf16", "f32", 2)
+    sess = Session(wl, TensorSource(wl))
+    z = torch.zeros((4, 256), dtype=torch.bfloat16, device="cuda")
+    gg = torch.zeros((4, 64), dtype=torch.bfloat16, device="cuda")
+    x = torch.zeros((2, 256), dtype=torch.bfloat16, device="cuda")
+    g = R.make_group(WRITE, 0, 1)
+    # x without y (or y without x) is rejected before anything is marked dirty
+    st = R.rwttt_write(sess.ctx, g, R.u32_array([0]), 0, 4, [z.data_ptr()], [gg.data_ptr()],
+                       0.1, x.data_ptr(), 0)
+    assert st == R.RWTTT_E_INVALID
+    assert sess.version(0) == (0, False)
+
+
 def test_injected_write_failure_rolls_back_exactly():
     wl = small_workload(520, 264, "bf16", "f32", 3)
     src = TensorSource(wl)
