@@ -165,6 +165,28 @@ rwttt_status rwttt_plan(const rwttt_ctx* ctx, const rwttt_event* ev, uint32_t n_
 rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
                         uint32_t layer, const void* x, void* y, void* stream);
 
+/* Tail buffers (TailBufferState, Section 4.1; TailBufferUpdate, Section 4.2
+ * primitives table and "READ"): request-local update evidence, the inputs x
+ * of the steps since the owner's last update boundary, kept for the next
+ * WRITE.  `tail` is a host array of n_owners * n_layers device pointers
+ * (index owner * n_layers + layer), each to `rows` x d_ff elements of the io
+ * dtype, row-major, 16-byte aligned, owned by the caller and disjoint from
+ * every other buffer.  Attaching (again) sets every tail length to 0.
+ * Errors: RWTTT_E_INVALID for null or misaligned pointers or rows == 0. */
+rwttt_status rwttt_attach_tail(rwttt_ctx* ctx, void* const* tail, uint32_t rows);
+
+/* Rows currently held in the tail of (owner, layer). */
+rwttt_status rwttt_tail_len(const rwttt_ctx* ctx, uint32_t owner, uint32_t layer, uint32_t* len);
+
+/* READ with TailBufferUpdate fused (Section 4.2 primitives table, phase R):
+ * rwttt_read, and in the same kernel the owner's x row is appended to the tail
+ * of (owner, layer) at row tail_len, which then grows by one.  No version
+ * changes (the tail is metadata, not a published state).  Errors, checked for
+ * every owner before anything is launched: RWTTT_E_INVALID if no tail is
+ * attached; RWTTT_E_CAPACITY if a tail is full. */
+rwttt_status rwttt_read_append(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
+                               uint32_t layer, const void* x, void* y, void* stream);
+
 /* WRITE / BoundaryUpdate (Section 3, Write; Section 4.2 "WRITE"): for each
  * slot b, owner r = owner_map[first+b]:
  *     shadow_{r,layer} = live_{r,layer} + eta * Z_b^T G_b
@@ -181,6 +203,11 @@ rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t
  * evidence and chunk <= 64 the token is fused into the update kernel, which
  * reads the live state once for both; otherwise the library runs a READ of
  * the group first.  Pass x = y = NULL for a WRITE without a token (prefill).
+ *
+ * With z == NULL the evidence rows come from the tail: the chunk is the
+ * owner's tail_len rows followed by this step's own input x (the WRITE step
+ * is the chunk's last token), so chunk must equal tail_len + 1 for every
+ * owner and x, y must be given.  The step's x is appended to the tail first.
  *
  * Marks each owner dirty (its write view is open until commit or rollback,
  * Section 4.1).  Errors: RWTTT_E_INVALID if only one of x, y is given;
@@ -199,13 +226,15 @@ rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_
  * validated first: RWTTT_E_NOT_DIRTY (no candidate), RWTTT_E_WRITE_FAILED
  * (its WRITE failed), RWTTT_E_OWNER_ALIAS (listed twice).  Later launches see
  * the new live slot; they must be ordered after the WRITE on the device (same
- * stream, or an event wait). */
+ * stream, or an event wait).  The update boundary is closed: the owner's
+ * tails become empty. */
 rwttt_status rwttt_commit(rwttt_ctx* ctx, const uint32_t* owners, uint32_t n);
 
 /* Rollback (Section 4.2 CONTROL; the failure branch of Algorithm 1): forget
  * each owner's candidate.  The live slots and V(r) are untouched, so version
- * v is restored exactly.  Errors as for commit, except that failed owners are
- * accepted. */
+ * v is restored exactly.  The chunk's evidence is dropped with it: the
+ * owner's tails become empty.  Errors as for commit, except that failed
+ * owners are accepted. */
 rwttt_status rwttt_rollback(rwttt_ctx* ctx, const uint32_t* owners, uint32_t n);
 
 /* View (Algorithm 1): committed version, and whether a candidate is open. */

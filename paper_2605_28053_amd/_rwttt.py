@@ -72,6 +72,9 @@ def _load():
                              P(rwttt_group), U32, P(U32), P(U32), U32, P(U32),
                              P(U32), U32, P(U32), P(I32)]),
         "rwttt_read": (I32, [VP, P(rwttt_group), P(U32), U32, VP, VP, VP]),
+        "rwttt_read_append": (I32, [VP, P(rwttt_group), P(U32), U32, VP, VP, VP]),
+        "rwttt_attach_tail": (I32, [VP, P(VP), U32]),
+        "rwttt_tail_len": (I32, [VP, U32, U32, P(U32)]),
         "rwttt_write": (I32, [VP, P(rwttt_group), P(U32), U32, U32, P(VP), P(VP), C.c_float,
                               VP, VP, VP]),
         "rwttt_commit": (I32, [VP, P(U32), U32]),
@@ -186,11 +189,30 @@ def rwttt_read(ctx, group, owner_map, layer, x_ptr, y_ptr, stream=0):
                            int(stream) or None)
 
 
+def rwttt_read_append(ctx, group, owner_map, layer, x_ptr, y_ptr, stream=0):
+    return _lib.rwttt_read_append(ctx, C.byref(group), owner_map, int(layer), int(x_ptr),
+                                  int(y_ptr), int(stream) or None)
+
+
+def rwttt_attach_tail(ctx, tail_ptrs, rows):
+    arr = (C.c_void_p * max(1, len(tail_ptrs)))(*[int(p) for p in tail_ptrs])
+    return _lib.rwttt_attach_tail(ctx, arr, int(rows))
+
+
+def rwttt_tail_len(ctx, owner, layer):
+    n = C.c_uint32(0)
+    st = _lib.rwttt_tail_len(ctx, int(owner), int(layer), C.byref(n))
+    if st != RWTTT_OK:
+        raise RwtttError(st, "rwttt_tail_len")
+    return n.value
+
+
 def rwttt_write(ctx, group, owner_map, layer, chunk, z_ptrs, g_ptrs, eta, x_ptr=0, y_ptr=0,
                 stream=0):
-    """x_ptr/y_ptr: the WRITE step's owner-indexed token input/output (0: no token)."""
-    n = len(z_ptrs)
-    z = (C.c_void_p * max(1, n))(*[int(p) for p in z_ptrs])
+    """x_ptr/y_ptr: the WRITE step's owner-indexed token input/output (0: no token).
+    z_ptrs=None: the chunk is the owners' tails plus this step's x."""
+    n = len(g_ptrs)
+    z = None if z_ptrs is None else (C.c_void_p * max(1, n))(*[int(p) for p in z_ptrs])
     g = (C.c_void_p * max(1, n))(*[int(p) for p in g_ptrs])
     return _lib.rwttt_write(ctx, C.byref(group), owner_map, int(layer), int(chunk), z, g,
                             float(eta), int(x_ptr) or None, int(y_ptr) or None,

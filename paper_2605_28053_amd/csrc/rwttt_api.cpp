@@ -20,12 +20,24 @@ struct rwttt_ctx {
   std::vector<uint8_t> dirty;        // [n_owners]: a candidate is open
   std::vector<uint8_t> failed;       // [n_owners]: a WRITE of the open candidate failed
   std::vector<uint32_t> mark;        // [n_owners]: alias detection, epoch-stamped
+  std::vector<void*> tail;           // [n_owners * n_layers] tail buffers, or empty
+  std::vector<uint32_t> tail_len;    // [n_owners * n_layers] rows held
+  uint32_t tail_rows = 0;
   uint32_t epoch = 0;
   uint32_t inject_failures = 0;
   int32_t last_hip = 0;
   rwttt::ReadGeometry geo{};
 
   size_t li(uint32_t owner, uint32_t layer) const { return size_t(owner) * cfg.n_layers + layer; }
+  size_t io_bytes() const { return cfg.io_dtype == RWTTT_BF16 ? 2 : 4; }
+  void* tail_row(uint32_t owner, uint32_t layer, uint32_t row) const {
+    return static_cast<char*>(tail[li(owner, layer)]) + size_t(row) * cfg.d_ff * io_bytes();
+  }
+  // An update boundary closed (commit or rollback): the owner's tails empty.
+  void clear_tail(uint32_t owner) {
+    if (tail.empty()) return;
+    for (uint32_t l = 0; l < cfg.n_layers; ++l) tail_len[li(owner, l)] = 0;
+  }
   void* slot(uint32_t owner, uint32_t layer, int which) const {
     const int s = live[li(owner, layer)] ^ which;
     return slots[li(owner, layer) * 2 + s];
@@ -243,8 +255,10 @@ rwttt_status rwttt_plan(const rwttt_ctx* ctx, const rwttt_event* ev, uint32_t n_
   return RWTTT_OK;
 }
 
-rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
-                        uint32_t layer, const void* x, void* y, void* stream) {
+namespace {
+
+rwttt_status read_impl(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
+                       uint32_t layer, const void* x, void* y, void* stream, bool append) {
   if (!ctx || !group) return RWTTT_E_INVALID;
   if (group->effect != RWTTT_READ && group->effect != RWTTT_WRITE) return RWTTT_E_INVALID;
   const uint32_t n = group->count;
@@ -255,6 +269,11 @@ rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t
   rwttt_status why = RWTTT_OK;
   if (!ctx->distinct_owners(owners, n, &why)) return why;
   if (!ctx->cfg.workspace) return RWTTT_E_INVALID;
+  if (append) {
+    if (ctx->tail.empty() || !aligned16(x)) return RWTTT_E_INVALID;
+    for (uint32_t b = 0; b < n; ++b)
+      if (ctx->tail_len[ctx->li(owners[b], layer)] >= ctx->tail_rows) return RWTTT_E_CAPACITY;
+  }
 
   rwttt::ReadLaunch L;
   L.io_bf16 = ctx->cfg.io_dtype == RWTTT_BF16;
@@ -268,11 +287,44 @@ rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t
   L.w0 = ctx->w0[layer];
   L.workspace = ctx->cfg.workspace;
   for (uint32_t b = 0; b < n; ++b) {
-    L.dw[b] = ctx->slot(owners[b], layer, 0);
-    L.row[b] = owners[b];
+    const uint32_t r = owners[b];
+    L.dw[b] = ctx->slot(r, layer, 0);
+    L.row[b] = r;
+    L.tail[b] = append ? ctx->tail_row(r, layer, ctx->tail_len[ctx->li(r, layer)]) : nullptr;
   }
   const hipError_t e = rwttt::launch_read(L, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(ctx, e);
+  if (append)
+    for (uint32_t b = 0; b < n; ++b) ++ctx->tail_len[ctx->li(owners[b], layer)];
+  return RWTTT_OK;
+}
+
+}  // namespace
+
+rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
+                        uint32_t layer, const void* x, void* y, void* stream) {
+  return read_impl(ctx, group, owner_map, layer, x, y, stream, false);
+}
+
+rwttt_status rwttt_read_append(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
+                               uint32_t layer, const void* x, void* y, void* stream) {
+  return read_impl(ctx, group, owner_map, layer, x, y, stream, true);
+}
+
+rwttt_status rwttt_attach_tail(rwttt_ctx* ctx, void* const* tail, uint32_t rows) {
+  if (!ctx || !tail || rows == 0 || rows > (1u << 20)) return RWTTT_E_INVALID;
+  const size_t nl = size_t(ctx->cfg.n_owners) * ctx->cfg.n_layers;
+  for (size_t i = 0; i < nl; ++i)
+    if (!tail[i] || !aligned16(tail[i])) return RWTTT_E_INVALID;
+  ctx->tail.assign(tail, tail + nl);
+  ctx->tail_len.assign(nl, 0);
+  ctx->tail_rows = rows;
+  return RWTTT_OK;
+}
+
+rwttt_status rwttt_tail_len(const rwttt_ctx* ctx, uint32_t owner, uint32_t layer, uint32_t* len) {
+  if (!ctx || !len || owner >= ctx->cfg.n_owners || layer >= ctx->cfg.n_layers) return RWTTT_E_INVALID;
+  *len = ctx->tail.empty() ? 0u : ctx->tail_len[ctx->li(owner, layer)];
   return RWTTT_OK;
 }
 
@@ -283,8 +335,10 @@ rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_
   if (group->effect != RWTTT_WRITE) return RWTTT_E_KEY_MISMATCH;
   const uint32_t n = group->count;
   if (n == 0) return RWTTT_OK;
-  if (!owner_map || !z || !g || layer >= ctx->cfg.n_layers || chunk == 0) return RWTTT_E_INVALID;
+  if (!owner_map || !g || layer >= ctx->cfg.n_layers || chunk == 0) return RWTTT_E_INVALID;
   if ((x == nullptr) != (y == nullptr)) return RWTTT_E_INVALID;
+  const bool from_tail = z == nullptr;
+  if (from_tail && (ctx->tail.empty() || !x || chunk > ctx->tail_rows)) return RWTTT_E_INVALID;
   if (x && (!ctx->cfg.workspace || !aligned16(x) || !aligned16(y))) return RWTTT_E_INVALID;
   if (chunk > (1u << 20)) return RWTTT_E_INVALID;
   if (n > ctx->cfg.max_group) return RWTTT_E_CAPACITY;
@@ -292,8 +346,10 @@ rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_
   rwttt_status why = RWTTT_OK;
   if (!ctx->distinct_owners(owners, n, &why)) return why;
   for (uint32_t b = 0; b < n; ++b) {
-    if (!z[b] || !g[b] || !aligned16(z[b]) || !aligned16(g[b])) return RWTTT_E_INVALID;
+    if (!g[b] || !aligned16(g[b])) return RWTTT_E_INVALID;
+    if (!from_tail && (!z[b] || !aligned16(z[b]))) return RWTTT_E_INVALID;
     const uint32_t r = owners[b];
+    if (from_tail && ctx->tail_len[ctx->li(r, layer)] + 1 != chunk) return RWTTT_E_INVALID;
     if (ctx->failed[r]) return RWTTT_E_WRITE_FAILED;
     if (ctx->written[ctx->li(r, layer)]) return RWTTT_E_DIRTY;
   }
@@ -326,11 +382,27 @@ rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_
   for (uint32_t b = 0; b < n; ++b) {
     L.live[b] = ctx->slot(owners[b], layer, 0);
     L.shadow[b] = ctx->slot(owners[b], layer, 1);
-    L.z[b] = z[b];
+    L.z[b] = from_tail ? ctx->tail[ctx->li(owners[b], layer)] : z[b];
     L.g[b] = g[b];
     L.row[b] = owners[b];
   }
-  const hipError_t e = rwttt::launch_write(L, static_cast<hipStream_t>(stream));
+  hipError_t e = hipSuccess;
+  if (from_tail) {
+    // the WRITE step's own input is the chunk's last row
+    rwttt::TailLaunch T;
+    T.io_bf16 = L.io_bf16;
+    T.d_ff = L.d_ff;
+    T.count = L.count;
+    T.x = x;
+    for (uint32_t b = 0; b < n; ++b) {
+      T.dst[b] = ctx->tail_row(owners[b], layer, chunk - 1);
+      T.row[b] = owners[b];
+    }
+    e = rwttt::launch_tail_append(T, static_cast<hipStream_t>(stream));
+    if (e == hipSuccess)
+      for (uint32_t b = 0; b < n; ++b) ctx->tail_len[ctx->li(owners[b], layer)] = chunk;
+  }
+  if (e == hipSuccess) e = rwttt::launch_write(L, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) {
     for (uint32_t b = 0; b < n; ++b) ctx->failed[owners[b]] = 1;
     return hip_fail(ctx, e);
@@ -357,6 +429,7 @@ rwttt_status rwttt_commit(rwttt_ctx* ctx, const uint32_t* owners, uint32_t n) {
     }
     ctx->version[r] += 1;
     ctx->dirty[r] = 0;
+    ctx->clear_tail(r);
   }
   return RWTTT_OK;
 }
@@ -372,6 +445,7 @@ rwttt_status rwttt_rollback(rwttt_ctx* ctx, const uint32_t* owners, uint32_t n) 
     for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l) ctx->written[ctx->li(r, l)] = 0;
     ctx->dirty[r] = 0;
     ctx->failed[r] = 0;
+    ctx->clear_tail(r);
   }
   return RWTTT_OK;
 }

@@ -42,6 +42,15 @@ struct ReadLaunch {
   void* workspace;           // ReadGeometry layout
   const void* dw[RWTTT_MAX_GROUP];   // live slot of each group slot
   uint32_t row[RWTTT_MAX_GROUP];     // owner id of each group slot
+  void* tail[RWTTT_MAX_GROUP];       // tail row that receives the slot's x row, or null
+};
+
+// Copy each group slot's x row (owner-indexed, d_ff io elements) to dst[b].
+struct TailLaunch {
+  int io_bf16, d_ff, count;
+  const void* x;
+  void* dst[RWTTT_MAX_GROUP];
+  uint32_t row[RWTTT_MAX_GROUP];
 };
 
 struct WriteLaunch {
@@ -60,6 +69,7 @@ struct WriteLaunch {
 };
 
 hipError_t launch_read(const ReadLaunch& L, hipStream_t stream);
+hipError_t launch_tail_append(const TailLaunch& L, hipStream_t stream);
 hipError_t launch_write(const WriteLaunch& L, hipStream_t stream);
 
 }  // namespace rwttt

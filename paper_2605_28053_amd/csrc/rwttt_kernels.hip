@@ -114,6 +114,7 @@ struct ReadParams {
   int count, d_ff, d_model, ks, nt, npad;
   const void* dw[RWTTT_MAX_GROUP];
   uint32_t row[RWTTT_MAX_GROUP];
+  void* tail[RWTTT_MAX_GROUP];     // TailBufferUpdate: row receiving x, or null
 };
 
 constexpr int kUnroll = 8;
@@ -185,6 +186,12 @@ __global__ void __launch_bounds__(kReadThreads) read_partial_kernel(const ReadPa
 
   for (int k = tid; k < KC; k += kReadThreads)
     xs[k] = k < kn ? Elem<IO>::get(p.x, size_t(p.row[b]) * p.d_ff + k0 + k) : 0.f;
+  if (p.tail[b] != nullptr && nt == 0) {
+    // TailBufferUpdate: the first column tile's blocks append this chunk of x
+    const IO* xr = static_cast<const IO*>(p.x) + size_t(p.row[b]) * p.d_ff + k0;
+    IO* tr = static_cast<IO*>(p.tail[b]) + k0;
+    for (int k = tid; k < kn; k += kReadThreads) tr[k] = xr[k];
+  }
   __syncthreads();
 
   const int kw0 = wave * RW;
@@ -703,6 +710,23 @@ __global__ void __launch_bounds__(256) write_valu_kernel(const WriteParams p) {
   store_n<4>(shadow + size_t(m) * p.d_model + n, out);
 }
 
+// ---------------------------------------------------------------------------
+// TailBufferUpdate for a WRITE step: its own x row becomes the chunk's last
+// ---------------------------------------------------------------------------
+
+struct TailParams {
+  int n16;                         // 16-byte units per row
+  const uint4* x;                  // owner-indexed rows of n16 units
+  uint4* dst[RWTTT_MAX_GROUP];
+  uint32_t row[RWTTT_MAX_GROUP];
+};
+
+__global__ void __launch_bounds__(256) tail_append_kernel(const TailParams p) {
+  const int b = blockIdx.y;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < p.n16) p.dst[b][i] = p.x[size_t(p.row[b]) * p.n16 + i];
+}
+
 template <typename IO, typename ST>
 hipError_t launch_read_t(const ReadLaunch& L, hipStream_t stream) {
   const ReadGeometry g = read_geometry(L.d_ff, L.d_model, L.state_bf16, L.n_owners);
@@ -720,6 +744,7 @@ hipError_t launch_read_t(const ReadLaunch& L, hipStream_t stream) {
   for (int b = 0; b < RWTTT_MAX_GROUP; ++b) {
     p.dw[b] = b < L.count ? L.dw[b] : nullptr;
     p.row[b] = b < L.count ? L.row[b] : 0u;
+    p.tail[b] = b < L.count ? L.tail[b] : nullptr;
   }
   // (chunk, tile) pairs rounded up to a multiple of the 8 XCDs
   const unsigned pairs8 = unsigned((g.ks * g.nt + 7) / 8 * 8);
@@ -778,6 +803,7 @@ hipError_t launch_write_t(const WriteLaunch& L, hipStream_t stream) {
       for (int b = 0; b < RWTTT_MAX_GROUP; ++b) {
         q.dw[b] = nullptr;
         q.row[b] = b < L.count ? L.row[b] : 0u;
+        q.tail[b] = nullptr;
       }
       hipLaunchKernelGGL((read_reduce_kernel<uint16_t>), dim3((L.d_model + 255) / 256, L.count),
                          dim3(256), 0, stream, q);
@@ -802,6 +828,7 @@ hipError_t launch_write_t(const WriteLaunch& L, hipStream_t stream) {
     for (int b = 0; b < L.count; ++b) {
       R.dw[b] = L.live[b];
       R.row[b] = L.row[b];
+      R.tail[b] = nullptr;
     }
     const hipError_t e = L.io_bf16 ? launch_read_t<uint16_t, ST>(R, stream)
                                    : launch_read_t<float, ST>(R, stream);
@@ -846,6 +873,18 @@ hipError_t launch_read(const ReadLaunch& L, hipStream_t stream) {
   }
   return L.state_bf16 ? launch_read_t<float, uint16_t>(L, stream)
                       : launch_read_t<float, float>(L, stream);
+}
+
+hipError_t launch_tail_append(const TailLaunch& L, hipStream_t stream) {
+  TailParams p;
+  p.n16 = L.d_ff * (L.io_bf16 ? 2 : 4) / 16;
+  p.x = static_cast<const uint4*>(L.x);
+  for (int b = 0; b < RWTTT_MAX_GROUP; ++b) {
+    p.dst[b] = b < L.count ? static_cast<uint4*>(L.dst[b]) : nullptr;
+    p.row[b] = b < L.count ? L.row[b] : 0u;
+  }
+  hipLaunchKernelGGL(tail_append_kernel, dim3((p.n16 + 255) / 256, L.count), dim3(256), 0, stream, p);
+  return hipGetLastError();
 }
 
 hipError_t launch_write(const WriteLaunch& L, hipStream_t stream) {

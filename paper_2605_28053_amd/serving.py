@@ -3,9 +3,12 @@
 ``Session`` owns the device memory of one workload -- W0 per layer, two state
 slots per (owner, layer) and the library workspace -- and runs decode steps:
 View (committed versions) -> events -> rwttt_plan -> per layer, per group:
-rwttt_read (the step's token) and, for WRITE groups, rwttt_write -> commit or
-rollback of the WRITE owners.  Host code here only marshals arguments; every
-number is computed by the library's kernels.
+rwttt_read for READ groups, rwttt_write (update plus the step's token) for
+WRITE groups -> commit or rollback of the WRITE owners.  When a workload's
+update evidence is the chunk's own activations, the session attaches tail
+buffers: READ steps append x to them (rwttt_read_append) and a WRITE takes its
+chunk from the tail.  Host code here only marshals arguments; every number is
+computed by the library's kernels.
 """
 
 from dataclasses import dataclass
@@ -83,7 +86,7 @@ class Session:
     """Device-resident state of one workload plus the serving loop."""
 
     def __init__(self, wl, src=None, layers=None, max_group=None, device="cuda",
-                 init_state=True, init_w0=True):
+                 init_state=True, init_w0=True, tail_rows=None):
         self.wl = wl
         self.device = device
         self.layers = list(range(wl.n_layers)) if layers is None else list(layers)
@@ -113,6 +116,18 @@ class Session:
         cfg.workspace_bytes = ws_bytes
         self.cfg = cfg
         self.ctx = R.rwttt_create(cfg)
+        # tail buffers (TailBufferState) when Z is the chunk's own inputs
+        if tail_rows is None:
+            tail_rows = 0 if wl.z_abs else max((wl.chunk,) + tuple(wl.chunk_choices))
+        self.tail_rows = tail_rows
+        self.tails = []
+        if tail_rows:
+            self.tails = [[torch.zeros((tail_rows, K), dtype=iodt, device=device)
+                           for _ in self.layers] for _ in range(wl.n_owners)]
+            st = R.rwttt_attach_tail(self.ctx, [t.data_ptr() for row in self.tails for t in row],
+                                     tail_rows)
+            if st != R.RWTTT_OK:
+                raise R.RwtttError(st, "rwttt_attach_tail")
 
     def close(self):
         if self.ctx:
@@ -157,7 +172,8 @@ class Session:
 
         x_ptrs[i], y_ptrs[i]: device addresses of [n_owners, d_ff] inputs and
         [n_owners, d_model] outputs of local layer i.  zg_ptrs[r] =
-        (z_ptrs_per_layer, g_ptrs_per_layer) for each WRITE owner r.
+        (z_ptrs_per_layer, g_ptrs_per_layer) for each WRITE owner r (with tail
+        buffers attached the z pointers are not used).
 
         ``stream`` is one HIP stream handle for every launch, or a
         ``StreamPair``: READ groups then go on its read stream and WRITE groups
@@ -188,12 +204,13 @@ class Session:
                 need_token = emit
                 if is_write and not failed:
                     # the WRITE transition returns the step's token with the candidate
-                    zs = [zg_ptrs[r][0][i] for r in owners]
+                    zs = None if self.tails else [zg_ptrs[r][0][i] for r in owners]
                     gs = [zg_ptrs[r][1][i] for r in owners]
+                    tok = emit or bool(self.tails)
                     if timer is not None:
-                        timer.begin("write_token" if emit else "write", g.count, chunk, stream)
+                        timer.begin("write_token" if tok else "write", g.count, chunk, stream)
                     st = R.rwttt_write(self.ctx, g, plan.owner_map_c, i, chunk, zs, gs, wl.eta,
-                                       x_ptrs[i] if emit else 0, y_ptrs[i] if emit else 0,
+                                       x_ptrs[i] if tok else 0, y_ptrs[i] if tok else 0,
                                        stream)
                     if timer is not None:
                         timer.end()
@@ -204,10 +221,12 @@ class Session:
                         failed = True
                 if need_token:
                     # READ groups, and the layers of a WRITE group whose update failed:
-                    # the token at the unchanged version v
+                    # the token at the unchanged version v (a READ step also appends
+                    # its input to the owner's tail)
                     if timer is not None:
                         timer.begin("read", g.count, 0, stream)
-                    st = R.rwttt_read(self.ctx, g, plan.owner_map_c, i, x_ptrs[i], y_ptrs[i], stream)
+                    fn = R.rwttt_read_append if self.tails and not is_write else R.rwttt_read
+                    st = fn(self.ctx, g, plan.owner_map_c, i, x_ptrs[i], y_ptrs[i], stream)
                     if timer is not None:
                         timer.end()
                     if st != R.RWTTT_OK:

@@ -249,6 +249,80 @@ def test_write_token_argument_errors():
     assert sess.version(0) == (0, False)
 
 
+# --------------------------------------------------------------------------
+# TailBufferUpdate: READ steps append x; a WRITE takes its chunk from the tail
+# --------------------------------------------------------------------------
+
+TAIL_CASES = [
+    # io, state, chunk
+    ("bf16", "f32", 4),
+    ("bf16", "bf16", 17),
+    ("bf16", "f32", 70),      # large chunk: READ for the token, then the GEMM
+    ("f32", "f32", 4),        # fp32 evidence
+]
+
+
+@pytest.mark.parametrize("io,state,chunk", TAIL_CASES)
+def test_tail_append_then_write_from_tail(io, state, chunk):
+    d_ff, d_model, n_owners = 1000, 264, 4
+    wl = small_workload(d_ff, d_model, io, state, n_owners, eta=0.05)
+    say("tail", io, state, chunk)
+    src = TensorSource(wl)
+    sess = Session(wl, src, tail_rows=chunk + 2)
+    tdt = torch.float32 if io == "f32" else torch.bfloat16
+    readers = [0, 2, 3]
+    writers = [2, 0]
+    X = [draw((n_owners, d_ff), 1.0, io, wl.seed, (80, t)) for t in range(chunk)]
+    W0 = O.widen(src.w0(0), io)
+    for t in range(chunk - 1):
+        xd = to_device(X[t], io)
+        y = torch.zeros((n_owners, d_model), dtype=tdt, device="cuda")
+        g = R.make_group(READ, 0, len(readers))
+        assert R.rwttt_read_append(sess.ctx, g, R.u32_array(readers), 0, xd.data_ptr(),
+                                   y.data_ptr()) == R.RWTTT_OK
+        torch.cuda.synchronize()
+        if t == 0:
+            for r in readers:
+                ref = O.round_to(O.read_apply(O.widen(X[t][r], io), W0,
+                                              O.widen(src.dw_init(r, 0), state)), io)
+                assert O.max_rel_floor(host_f64(y[r], io), ref) <= out_tol(io)
+    for r in range(n_owners):
+        assert R.rwttt_tail_len(sess.ctx, r, 0) == (chunk - 1 if r in readers else 0)
+        # the tail holds the appended rows bit for bit
+        got = to_host(sess.tails[r][0][:chunk - 1], io)
+        if r in readers:
+            assert np.array_equal(got, np.stack([X[t][r] for t in range(chunk - 1)]))
+    assert sess.versions() == [0] * n_owners
+    # the WRITE step: Z = the tail rows, then this step's own x
+    xd = to_device(X[chunk - 1], io)
+    y = torch.zeros((n_owners, d_model), dtype=tdt, device="cuda")
+    Gs = {r: draw((chunk, d_model), 1.0, io, wl.seed, (81, r)) for r in writers}
+    gds = [to_device(Gs[r], io) for r in writers]
+    wg = R.make_group(WRITE, 0, len(writers))
+    assert R.rwttt_write(sess.ctx, wg, R.u32_array(writers), 0, chunk, None,
+                         [g.data_ptr() for g in gds], wl.eta, xd.data_ptr(), y.data_ptr(),
+                         stream=torch.cuda.current_stream().cuda_stream) == R.RWTTT_OK
+    torch.cuda.synchronize()
+    for r in writers:
+        Z = np.stack([X[t][r] for t in range(chunk)])
+        D0 = O.widen(src.dw_init(r, 0), state)
+        cand = O.round_to(O.write_candidate(D0, O.widen(Z, io), O.widen(Gs[r], io), wl.eta), state)
+        shadow = host_f64(sess.shadow(r, 0), state)
+        if state == "f32":
+            assert O.rel_frobenius(shadow, cand) <= STATE_TOL
+        else:
+            assert O.max_rel_floor(shadow, cand) <= BF16_OUT_TOL
+        ref = O.round_to(O.read_apply(O.widen(X[chunk - 1][r], io), W0, D0), io)
+        assert O.max_rel_floor(host_f64(y[r], io), ref) <= out_tol(io)
+        assert R.rwttt_tail_len(sess.ctx, r, 0) == chunk
+        assert np.array_equal(to_host(sess.tails[r][0][chunk - 1], io), X[chunk - 1][r])
+    # the boundary closes on commit and on rollback; other owners keep their tails
+    assert R.rwttt_commit(sess.ctx, [2]) == R.RWTTT_OK
+    assert R.rwttt_rollback(sess.ctx, [0]) == R.RWTTT_OK
+    assert [R.rwttt_tail_len(sess.ctx, r, 0) for r in range(n_owners)] == [0, 0, 0, chunk - 1]
+    assert sess.versions() == [0, 0, 1, 0]
+
+
 def test_injected_write_failure_rolls_back_exactly():
     wl = small_workload(520, 264, "bf16", "f32", 3)
     src = TensorSource(wl)

@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 16
     out = subprocess.run(["nm", "-D", "--defined-only", R.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (rwttt_\w+)", out))
@@ -134,6 +134,44 @@ def test_owner_table_state_machine_and_error_codes():
     assert R.rwttt_read(ctx, rg, R.u32_array([0]), 5, 0x1000, 0x2000) == R.RWTTT_E_INVALID
     ag = R.make_group(R.RWTTT_READ, 0, 2)
     assert R.rwttt_read(ctx, ag, R.u32_array([2, 2]), 0, 0x1000, 0x2000) == R.RWTTT_E_OWNER_ALIAS
+
+
+def test_tail_state_machine_and_errors_before_any_launch():
+    """Tail validation paths that return before the device is touched: the
+    workspace address below is never dereferenced."""
+    n_owners, n_layers, d_ff, d_model = 3, 2, 64, 32
+    w0 = [0x10000 * (i + 1) for i in range(n_layers)]
+    slots = [0x1000000 + 0x1000 * i for i in range(n_owners * n_layers * 2)]
+    cfg = R.make_config(n_owners, n_layers, d_ff, d_model, R.RWTTT_BF16, R.RWTTT_F32, 4, w0, slots)
+    ws = R.rwttt_workspace_bytes(cfg)
+    cfg = R.make_config(n_owners, n_layers, d_ff, d_model, R.RWTTT_BF16, R.RWTTT_F32, 4, w0, slots,
+                        workspace=0x40000000, workspace_bytes=ws)
+    ctx = R.rwttt_create(cfg)
+    rg = R.make_group(R.RWTTT_READ, 0, 1)
+    wg = R.make_group(R.RWTTT_WRITE, 0, 1)
+    one = R.u32_array([1])
+    # no tail attached
+    assert R.rwttt_read_append(ctx, rg, one, 0, 0x2000, 0x3000) == R.RWTTT_E_INVALID
+    assert R.rwttt_write(ctx, wg, one, 0, 1, None, [0x200], 1.0, 0x2000, 0x3000) == R.RWTTT_E_INVALID
+    assert R.rwttt_tail_len(ctx, 1, 0) == 0
+    tails = [0x2000000 + 0x1000 * i for i in range(n_owners * n_layers)]
+    assert R.rwttt_attach_tail(ctx, tails, 0) == R.RWTTT_E_INVALID
+    assert R.rwttt_attach_tail(ctx, tails[:-1] + [tails[-1] + 8], 4) == R.RWTTT_E_INVALID
+    assert R.rwttt_attach_tail(ctx, tails, 4) == R.RWTTT_OK
+    # a tail WRITE needs chunk == tail_len + 1, a token, and fits the tail
+    assert R.rwttt_write(ctx, wg, one, 0, 2, None, [0x200], 1.0, 0x2000, 0x3000) == R.RWTTT_E_INVALID
+    assert R.rwttt_write(ctx, wg, one, 0, 5, None, [0x200], 1.0, 0x2000, 0x3000) == R.RWTTT_E_INVALID
+    assert R.rwttt_write(ctx, wg, one, 0, 1, None, [0x200], 1.0) == R.RWTTT_E_INVALID
+    assert R.rwttt_version(ctx, 1) == (0, False)
+    # an injected failure opens the candidate without launching; rollback closes it
+    assert R.rwttt_inject_write_failures(ctx, 1) == R.RWTTT_OK
+    assert R.rwttt_write(ctx, wg, one, 0, 1, None, [0x200], 1.0, 0x2000, 0x3000) == R.RWTTT_E_WRITE_FAILED
+    assert R.rwttt_version(ctx, 1) == (0, True)
+    assert R.rwttt_rollback(ctx, [1]) == R.RWTTT_OK
+    assert R.rwttt_tail_len(ctx, 1, 0) == 0
+    with pytest.raises(R.RwtttError):
+        R.rwttt_tail_len(ctx, 3, 0)
+    R.rwttt_destroy(ctx)
 
 
 def test_slots_are_live_and_shadow_of_each_owner_layer():
