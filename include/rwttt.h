@@ -245,6 +245,37 @@ rwttt_status rwttt_version(const rwttt_ctx* ctx, uint32_t owner, uint64_t* versi
 rwttt_status rwttt_slot(const rwttt_ctx* ctx, uint32_t owner, uint32_t layer, int32_t which,
                         void** ptr);
 
+/* Fork (Section 4.2 CONTROL: fork creates a separate owner/version lineage):
+ * owner dst becomes a copy of owner src's committed state.  Every layer's
+ * live slot of src (version V(src)) is copied into dst's live slot, dst's
+ * tails receive src's tail rows and lengths, and V(dst) = V(src); from then
+ * on the two lineages advance independently.  src may hold an open
+ * candidate (it is not copied).  One kernel launch on `stream` copies all
+ * layers; it reads the slots that are live at enqueue time.  Errors:
+ * RWTTT_E_OWNER_ALIAS if src == dst; RWTTT_E_DIRTY if dst holds a candidate;
+ * RWTTT_E_INVALID if an owner id is out of range or there is no workspace
+ * (a host-only context). */
+rwttt_status rwttt_fork(rwttt_ctx* ctx, uint32_t src, uint32_t dst, void* stream);
+
+/* Checkpoint (Section 4.1 snapshot; Section 4.2 CONTROL): copy the owner's
+ * committed state, the live slot of every layer (d_ff x d_model state
+ * elements, row-major), into dst[layer] and return its version.  dst is a
+ * host array of n_layers caller-owned buffers, each pinned host memory (from
+ * hipHostMalloc) or device memory; the copies are asynchronous on `stream`
+ * (hipMemcpyAsync), so the caller synchronises before reading them.  An open
+ * candidate is allowed and not copied.  Errors: RWTTT_E_INVALID for a bad
+ * owner or a null buffer. */
+rwttt_status rwttt_checkpoint(rwttt_ctx* ctx, uint32_t owner, void* const* dst,
+                              uint64_t* version, void* stream);
+
+/* Resume from a checkpoint: copy src[layer] (as written by rwttt_checkpoint)
+ * into the owner's live slots, set V(owner) = version and empty its tails.
+ * Asynchronous on `stream`; later launches on the same stream see the
+ * restored state.  Errors: RWTTT_E_DIRTY if the owner holds a candidate;
+ * RWTTT_E_INVALID for a bad owner or a null buffer. */
+rwttt_status rwttt_resume(rwttt_ctx* ctx, uint32_t owner, const void* const* src,
+                          uint64_t version, void* stream);
+
 /* Failure injection for state-contract tests (Section 5.5): the next `count`
  * rwttt_write calls validate, mark their owners dirty and failed, launch
  * nothing and return RWTTT_E_WRITE_FAILED. */

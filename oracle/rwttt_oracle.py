@@ -247,6 +247,32 @@ class OwnerTable:
         self.dirty[r] = False
         return OK
 
+    def fork(self, src, dst):
+        """Owner dst starts a new lineage from src's committed state and
+        version (Section 4.2 CONTROL, fork); src's open candidate stays its own."""
+        if src == dst:
+            return E_OWNER_ALIAS
+        if self.dirty[dst]:
+            return E_DIRTY
+        for l in self.layers:
+            self.D[(dst, l)] = self.D[(src, l)].copy()
+        self.V[dst] = self.V[src]
+        return OK
+
+    def checkpoint(self, r):
+        """Owner r's committed state and version (the snapshot of Section 4.1)."""
+        return {l: self.D[(r, l)].copy() for l in self.layers}, self.V[r]
+
+    def resume(self, r, snap):
+        """Restore a checkpoint taken by checkpoint() into owner r."""
+        if self.dirty[r]:
+            return E_DIRTY
+        state, v = snap
+        for l in self.layers:
+            self.D[(r, l)] = state[l].copy()
+        self.V[r] = v
+        return OK
+
 
 @dataclass
 class StepRecord:

@@ -81,6 +81,9 @@ def _load():
         "rwttt_rollback": (I32, [VP, P(U32), U32]),
         "rwttt_version": (I32, [VP, U32, P(U64), P(I32)]),
         "rwttt_slot": (I32, [VP, U32, U32, I32, P(VP)]),
+        "rwttt_fork": (I32, [VP, U32, U32, VP]),
+        "rwttt_checkpoint": (I32, [VP, U32, P(VP), P(U64), VP]),
+        "rwttt_resume": (I32, [VP, U32, P(VP), U64, VP]),
         "rwttt_inject_write_failures": (I32, [VP, U32]),
         "rwttt_last_hip_error": (I32, [VP]),
         "rwttt_strerror": (C.c_char_p, [I32]),
@@ -243,6 +246,23 @@ def rwttt_slot(ctx, owner, layer, which):
     if st != RWTTT_OK:
         raise RwtttError(st, "rwttt_slot")
     return p.value
+
+
+def rwttt_fork(ctx, src, dst, stream=0):
+    return _lib.rwttt_fork(ctx, int(src), int(dst), int(stream) or None)
+
+
+def rwttt_checkpoint(ctx, owner, dst_ptrs, stream=0):
+    """Returns (status, version)."""
+    arr = (C.c_void_p * max(1, len(dst_ptrs)))(*[int(p) for p in dst_ptrs])
+    v = C.c_uint64(0)
+    st = _lib.rwttt_checkpoint(ctx, int(owner), arr, C.byref(v), int(stream) or None)
+    return st, v.value
+
+
+def rwttt_resume(ctx, owner, src_ptrs, version, stream=0):
+    arr = (C.c_void_p * max(1, len(src_ptrs)))(*[int(p) for p in src_ptrs])
+    return _lib.rwttt_resume(ctx, int(owner), arr, int(version), int(stream) or None)
 
 
 def rwttt_inject_write_failures(ctx, count):

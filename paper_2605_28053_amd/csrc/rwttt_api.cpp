@@ -450,6 +450,67 @@ rwttt_status rwttt_rollback(rwttt_ctx* ctx, const uint32_t* owners, uint32_t n) 
   return RWTTT_OK;
 }
 
+rwttt_status rwttt_fork(rwttt_ctx* ctx, uint32_t src, uint32_t dst, void* stream) {
+  if (!ctx || src >= ctx->cfg.n_owners || dst >= ctx->cfg.n_owners) return RWTTT_E_INVALID;
+  if (src == dst) return RWTTT_E_OWNER_ALIAS;
+  if (ctx->dirty[dst]) return RWTTT_E_DIRTY;
+  if (!ctx->cfg.workspace) return RWTTT_E_INVALID;
+  const size_t state_bytes = size_t(ctx->cfg.d_ff) * ctx->cfg.d_model *
+                             (ctx->cfg.state_dtype == RWTTT_BF16 ? 2 : 4);
+  std::vector<rwttt::CopyJob> jobs;
+  for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l) {
+    jobs.push_back({ctx->slot(src, l, 0), ctx->slot(dst, l, 0), state_bytes});
+    if (!ctx->tail.empty()) {
+      const uint32_t rows = ctx->tail_len[ctx->li(src, l)];
+      if (rows) jobs.push_back({ctx->tail[ctx->li(src, l)], ctx->tail[ctx->li(dst, l)],
+                                size_t(rows) * ctx->cfg.d_ff * ctx->io_bytes()});
+    }
+  }
+  const hipError_t e = rwttt::launch_copy(jobs.data(), int(jobs.size()),
+                                          static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(ctx, e);
+  ctx->version[dst] = ctx->version[src];
+  ctx->failed[dst] = 0;
+  if (!ctx->tail.empty())
+    for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l)
+      ctx->tail_len[ctx->li(dst, l)] = ctx->tail_len[ctx->li(src, l)];
+  return RWTTT_OK;
+}
+
+rwttt_status rwttt_checkpoint(rwttt_ctx* ctx, uint32_t owner, void* const* dst, uint64_t* version,
+                              void* stream) {
+  if (!ctx || !dst || !version || owner >= ctx->cfg.n_owners) return RWTTT_E_INVALID;
+  for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l)
+    if (!dst[l]) return RWTTT_E_INVALID;
+  const size_t state_bytes = size_t(ctx->cfg.d_ff) * ctx->cfg.d_model *
+                             (ctx->cfg.state_dtype == RWTTT_BF16 ? 2 : 4);
+  for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l) {
+    const hipError_t e = hipMemcpyAsync(dst[l], ctx->slot(owner, l, 0), state_bytes,
+                                        hipMemcpyDefault, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(ctx, e);
+  }
+  *version = ctx->version[owner];
+  return RWTTT_OK;
+}
+
+rwttt_status rwttt_resume(rwttt_ctx* ctx, uint32_t owner, const void* const* src, uint64_t version,
+                          void* stream) {
+  if (!ctx || !src || owner >= ctx->cfg.n_owners) return RWTTT_E_INVALID;
+  if (ctx->dirty[owner]) return RWTTT_E_DIRTY;
+  for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l)
+    if (!src[l]) return RWTTT_E_INVALID;
+  const size_t state_bytes = size_t(ctx->cfg.d_ff) * ctx->cfg.d_model *
+                             (ctx->cfg.state_dtype == RWTTT_BF16 ? 2 : 4);
+  for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l) {
+    const hipError_t e = hipMemcpyAsync(ctx->slot(owner, l, 0), src[l], state_bytes,
+                                        hipMemcpyDefault, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(ctx, e);
+  }
+  ctx->version[owner] = version;
+  ctx->clear_tail(owner);
+  return RWTTT_OK;
+}
+
 rwttt_status rwttt_version(const rwttt_ctx* ctx, uint32_t owner, uint64_t* version, int32_t* dirty) {
   if (!ctx || owner >= ctx->cfg.n_owners) return RWTTT_E_INVALID;
   if (version) *version = ctx->version[owner];

@@ -70,6 +70,14 @@ struct WriteLaunch {
 
 hipError_t launch_read(const ReadLaunch& L, hipStream_t stream);
 hipError_t launch_tail_append(const TailLaunch& L, hipStream_t stream);
+
+// Device-to-device copies of n 16-byte-aligned regions (one launch per 64).
+struct CopyJob {
+  const void* src;
+  void* dst;
+  size_t bytes;              // multiple of 16
+};
+hipError_t launch_copy(const CopyJob* jobs, int n, hipStream_t stream);
 hipError_t launch_write(const WriteLaunch& L, hipStream_t stream);
 
 }  // namespace rwttt

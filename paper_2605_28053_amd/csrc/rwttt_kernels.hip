@@ -727,6 +727,35 @@ __global__ void __launch_bounds__(256) tail_append_kernel(const TailParams p) {
   if (i < p.n16) p.dst[b][i] = p.x[size_t(p.row[b]) * p.n16 + i];
 }
 
+// ---------------------------------------------------------------------------
+// Fork: bulk copy of slots and tails (streaming, non-temporal both ways)
+// ---------------------------------------------------------------------------
+
+constexpr int kCopyJobs = 64;
+
+struct CopyParams {
+  const u32x4_t* src[kCopyJobs];
+  u32x4_t* dst[kCopyJobs];
+  size_t n16[kCopyJobs];
+};
+
+__global__ void __launch_bounds__(256) copy_kernel(const CopyParams p) {
+  const int j = blockIdx.y;
+  const size_t n = p.n16[j];
+  const u32x4_t* s = p.src[j];
+  u32x4_t* d = p.dst[j];
+  const size_t stride = size_t(gridDim.x) * 256 * 4;
+  for (size_t i = size_t(blockIdx.x) * 256 * 4 + threadIdx.x; i < n; i += stride) {
+    u32x4_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (i + size_t(u) * 256 < n) v[u] = __builtin_nontemporal_load(s + i + size_t(u) * 256);
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (i + size_t(u) * 256 < n) __builtin_nontemporal_store(v[u], d + i + size_t(u) * 256);
+  }
+}
+
 template <typename IO, typename ST>
 hipError_t launch_read_t(const ReadLaunch& L, hipStream_t stream) {
   const ReadGeometry g = read_geometry(L.d_ff, L.d_model, L.state_bf16, L.n_owners);
@@ -885,6 +914,27 @@ hipError_t launch_tail_append(const TailLaunch& L, hipStream_t stream) {
   }
   hipLaunchKernelGGL(tail_append_kernel, dim3((p.n16 + 255) / 256, L.count), dim3(256), 0, stream, p);
   return hipGetLastError();
+}
+
+hipError_t launch_copy(const CopyJob* jobs, int n, hipStream_t stream) {
+  for (int first = 0; first < n; first += kCopyJobs) {
+    const int m = std::min(kCopyJobs, n - first);
+    CopyParams p;
+    size_t most = 0;
+    for (int j = 0; j < kCopyJobs; ++j) {
+      const bool in = j < m;
+      p.src[j] = in ? static_cast<const u32x4_t*>(jobs[first + j].src) : nullptr;
+      p.dst[j] = in ? static_cast<u32x4_t*>(jobs[first + j].dst) : nullptr;
+      p.n16[j] = in ? jobs[first + j].bytes / 16 : 0;
+      most = std::max(most, p.n16[j]);
+    }
+    if (most == 0) continue;
+    const size_t blocks = std::min<size_t>((most + 1023) / 1024, 2048);
+    hipLaunchKernelGGL(copy_kernel, dim3(unsigned(blocks), unsigned(m)), dim3(256), 0, stream, p);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_write(const WriteLaunch& L, hipStream_t stream) {

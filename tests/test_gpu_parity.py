@@ -323,6 +323,98 @@ def test_tail_append_then_write_from_tail(io, state, chunk):
     assert sess.versions() == [0, 0, 1, 0]
 
 
+# --------------------------------------------------------------------------
+# Fork, checkpoint and resume (Section 4.2 CONTROL; Section 4.1 snapshot)
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("state", ["f32", "bf16"])
+def test_fork_checkpoint_resume_match_oracle(state):
+    d_ff, d_model, n_owners, L = 1000, 264, 4, 2
+    base = small_workload(d_ff, d_model, "bf16", state, n_owners, eta=0.05)
+    import dataclasses
+    wl = dataclasses.replace(base, n_layers=L)
+    say("fork/checkpoint", state)
+    src = TensorSource(wl)
+    sess = Session(wl, src)
+    table = O.OwnerTable(n_owners, range(L))
+    for r in range(n_owners):
+        for l in range(L):
+            table.D[(r, l)] = O.widen(src.dw_init(r, l), state)
+    chunk = 16
+
+    def write_commit(owners, key):
+        zs = {l: [] for l in range(L)}
+        gs = {l: [] for l in range(L)}
+        for r in owners:
+            for l in range(L):
+                Z = draw((chunk, d_ff), 1.0, "bf16", wl.seed, (key, r, l), absval=True)
+                G = draw((chunk, d_model), 1.0, "bf16", wl.seed, (key + 1, r, l))
+                zs[l].append(to_device(Z, "bf16"))
+                gs[l].append(to_device(G, "bf16"))
+                table.cand[(r, l)] = O.round_to(O.write_candidate(
+                    table.D[(r, l)], O.widen(Z, "bf16"), O.widen(G, "bf16"), wl.eta), state)
+            table.dirty[r] = True
+        for l in range(L):
+            assert write_group(sess, owners, l, chunk, zs[l], gs[l]) == R.RWTTT_OK
+        assert R.rwttt_commit(sess.ctx, owners) == R.RWTTT_OK
+        for r in owners:
+            assert table.commit(r) == O.OK
+        torch.cuda.synchronize()
+
+    def check_state(r):
+        for l in range(L):
+            got = host_f64(sess.live(r, l), state)
+            assert O.rel_frobenius(got, table.D[(r, l)]) <= STATE_TOL, (r, l)
+
+    write_commit([0, 1], 90)
+    # fork 0 -> 2: live slots bit-identical, versions equal, READs bit-identical
+    assert R.rwttt_fork(sess.ctx, 0, 2, torch.cuda.current_stream().cuda_stream) == R.RWTTT_OK
+    assert table.fork(0, 2) == O.OK
+    torch.cuda.synchronize()
+    assert sess.versions() == table.V == [1, 1, 1, 0]
+    for l in range(L):
+        assert slot_hash(sess.live(2, l)) == slot_hash(sess.live(0, l))
+    x = to_device(draw((n_owners, d_ff), 1.0, "bf16", wl.seed, (92,)), "bf16")
+    y = torch.zeros((n_owners, d_model), dtype=torch.bfloat16, device="cuda")
+    X = draw((n_owners, d_ff), 1.0, "bf16", wl.seed, (92,))
+    x[2] = x[0]
+    read_group(sess, [0, 2], 1, x, y)
+    torch.cuda.synchronize()
+    assert torch.equal(y[0], y[2])
+    # checkpoint owner 1 to pinned host memory, then move it on and resume
+    nbytes = sess.live(1, 0).numel() * sess.live(1, 0).element_size()
+    host = [torch.empty(nbytes, dtype=torch.uint8, pin_memory=True) for _ in range(L)]
+    st, v = R.rwttt_checkpoint(sess.ctx, 1, [h.data_ptr() for h in host],
+                               torch.cuda.current_stream().cuda_stream)
+    assert st == R.RWTTT_OK and v == 1
+    snap = table.checkpoint(1)
+    torch.cuda.synchronize()
+    hashes = [slot_hash(sess.live(1, l)) for l in range(L)]
+    # the lineages are separate: writes to the child and the parent stay local
+    write_commit([2], 94)
+    write_commit([0, 1], 96)
+    assert sess.versions() == table.V == [2, 2, 2, 0]
+    for r in range(n_owners):
+        check_state(r)
+    assert R.rwttt_resume(sess.ctx, 1, [h.data_ptr() for h in host], v,
+                          torch.cuda.current_stream().cuda_stream) == R.RWTTT_OK
+    assert table.resume(1, snap) == O.OK
+    torch.cuda.synchronize()
+    assert sess.versions() == table.V == [2, 1, 2, 0]
+    assert [slot_hash(sess.live(1, l)) for l in range(L)] == hashes
+    check_state(1)
+    # READ outputs of every owner against the oracle
+    xd = to_device(X, "bf16")
+    y = torch.zeros((n_owners, d_model), dtype=torch.bfloat16, device="cuda")
+    for l in range(L):
+        read_group(sess, list(range(n_owners)), l, xd, y)
+        torch.cuda.synchronize()
+        W0 = O.widen(src.w0(l), "bf16")
+        for r in range(n_owners):
+            ref = O.round_to(O.read_apply(O.widen(X[r], "bf16"), W0, table.D[(r, l)]), "bf16")
+            assert O.max_rel_floor(host_f64(y[r], "bf16"), ref) <= BF16_OUT_TOL, (r, l)
+
+
 def test_injected_write_failure_rolls_back_exactly():
     wl = small_workload(520, 264, "bf16", "f32", 3)
     src = TensorSource(wl)

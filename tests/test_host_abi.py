@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 16
+    assert len(names) == 19
     out = subprocess.run(["nm", "-D", "--defined-only", R.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (rwttt_\w+)", out))
@@ -171,6 +171,23 @@ def test_tail_state_machine_and_errors_before_any_launch():
     assert R.rwttt_tail_len(ctx, 1, 0) == 0
     with pytest.raises(R.RwtttError):
         R.rwttt_tail_len(ctx, 3, 0)
+    R.rwttt_destroy(ctx)
+
+
+def test_fork_checkpoint_resume_validation():
+    ctx, _ = host_ctx(n_owners=4, n_layers=2)
+    assert R.rwttt_fork(ctx, 1, 1) == R.RWTTT_E_OWNER_ALIAS
+    assert R.rwttt_fork(ctx, 1, 7) == R.RWTTT_E_INVALID
+    make_dirty(ctx, [2])
+    assert R.rwttt_fork(ctx, 1, 2) == R.RWTTT_E_DIRTY
+    assert R.rwttt_resume(ctx, 2, [0x5000, 0x6000], 3) == R.RWTTT_E_DIRTY
+    # no workspace: a host-only context refuses the device copy
+    assert R.rwttt_fork(ctx, 1, 3) == R.RWTTT_E_INVALID
+    assert R.rwttt_checkpoint(ctx, 9, [0x5000, 0x6000])[0] == R.RWTTT_E_INVALID
+    assert R.rwttt_checkpoint(ctx, 1, [0x5000, 0])[0] == R.RWTTT_E_INVALID
+    assert R.rwttt_resume(ctx, 1, [0, 0x6000], 3) == R.RWTTT_E_INVALID
+    assert R.rwttt_version(ctx, 1) == (0, False)
+    assert R.rwttt_rollback(ctx, [2]) == R.RWTTT_OK
     R.rwttt_destroy(ctx)
 
 

@@ -492,3 +492,36 @@ def test_inputs_are_seeded_and_blockwise_reproducible():
         assert sum(i.effect == WRITE for i in items) == 8
         assert len({i.owner for i in items}) == 24
         assert all(i.chunk in (16, 32, 64) for i in items if i.effect == WRITE)
+
+
+def test_fork_checkpoint_resume_are_independent_copies():
+    """Fork starts a separate lineage (Section 4.2 CONTROL): the child equals the
+    parent at the fork, and later commits on either side stay on that side.
+    A checkpoint restores state and version exactly (Section 4.1 snapshot)."""
+    wl = workload(0)
+    trace, src = build_trace(wl), TensorSource(wl)
+    records, table = O.run_trace(wl, trace, src, steps=range(8))
+    assert table.V == [2, 2]
+    W0 = O.widen(src.w0(0), "f32")
+    x = O.widen(src.x(8, 0, 0), "f32")
+    before1 = table.D[(1, 0)].copy()
+    assert table.fork(0, 0) == O.E_OWNER_ALIAS
+    snap = table.checkpoint(0)
+    assert table.fork(0, 1) == O.OK
+    assert table.V[1] == table.V[0] and np.array_equal(table.D[(1, 0)], table.D[(0, 0)])
+    assert not np.array_equal(table.D[(1, 0)], before1)
+    assert np.array_equal(O.read_apply(x, W0, table.D[(1, 0)]), O.read_apply(x, W0, table.D[(0, 0)]))
+    # a commit on the parent leaves the child at the fork point
+    child = table.D[(1, 0)].copy()
+    Z, G = src.zg(11, 0, 0, 4)
+    table.cand[(0, 0)] = O.write_candidate(table.D[(0, 0)], O.widen(Z, "f32"), O.widen(G, "f32"), wl.eta)
+    table.dirty[0] = True
+    assert table.fork(1, 0) == O.E_DIRTY
+    assert table.resume(0, snap) == O.E_DIRTY
+    assert table.commit(0) == O.OK
+    assert table.V == [3, 2]
+    assert np.array_equal(table.D[(1, 0)], child)
+    assert not np.array_equal(table.D[(0, 0)], child)
+    # resume returns the parent to its checkpoint, exactly
+    assert table.resume(0, snap) == O.OK
+    assert table.V[0] == 2 and np.array_equal(table.D[(0, 0)], child)
