@@ -103,7 +103,9 @@ typedef struct rwttt_config {
                                    Slot 0 holds version 0 and starts live.       */
     void* workspace;            /* device buffer of rwttt_workspace_bytes() bytes,
                                    or NULL for a host-only context (planning and
-                                   the owner table; rwttt_read/_write then fail) */
+                                   the owner table): every call that would touch
+                                   the device (read, write, fork, checkpoint,
+                                   resume) then returns RWTTT_E_INVALID */
     size_t workspace_bytes;
 } rwttt_config;
 

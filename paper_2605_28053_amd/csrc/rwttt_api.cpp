@@ -353,6 +353,8 @@ rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_
     if (ctx->failed[r]) return RWTTT_E_WRITE_FAILED;
     if (ctx->written[ctx->li(r, layer)]) return RWTTT_E_DIRTY;
   }
+  // a host-only context launches nothing; only an injected failure may open a candidate there
+  if (!ctx->cfg.workspace && ctx->inject_failures == 0) return RWTTT_E_INVALID;
 
   // The write view is open from here until commit or rollback.
   for (uint32_t b = 0; b < n; ++b) {
@@ -480,6 +482,7 @@ rwttt_status rwttt_fork(rwttt_ctx* ctx, uint32_t src, uint32_t dst, void* stream
 rwttt_status rwttt_checkpoint(rwttt_ctx* ctx, uint32_t owner, void* const* dst, uint64_t* version,
                               void* stream) {
   if (!ctx || !dst || !version || owner >= ctx->cfg.n_owners) return RWTTT_E_INVALID;
+  if (!ctx->cfg.workspace) return RWTTT_E_INVALID;   // host-only context: no device copies
   for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l)
     if (!dst[l]) return RWTTT_E_INVALID;
   const size_t state_bytes = size_t(ctx->cfg.d_ff) * ctx->cfg.d_model *
@@ -497,6 +500,7 @@ rwttt_status rwttt_resume(rwttt_ctx* ctx, uint32_t owner, const void* const* src
                           void* stream) {
   if (!ctx || !src || owner >= ctx->cfg.n_owners) return RWTTT_E_INVALID;
   if (ctx->dirty[owner]) return RWTTT_E_DIRTY;
+  if (!ctx->cfg.workspace) return RWTTT_E_INVALID;   // host-only context: no device copies
   for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l)
     if (!src[l]) return RWTTT_E_INVALID;
   const size_t state_bytes = size_t(ctx->cfg.d_ff) * ctx->cfg.d_model *

@@ -128,6 +128,8 @@ def test_owner_table_state_machine_and_error_codes():
     assert R.rwttt_rollback(ctx, [0]) == R.RWTTT_OK
     # no workspace: device calls are refused, nothing is launched
     assert R.rwttt_read(ctx, rg, R.u32_array([0]), 0, 0x1000, 0x2000) == R.RWTTT_E_INVALID
+    assert R.rwttt_write(ctx, wg, R.u32_array([3]), 0, 4, [0x100], [0x200], 1.0) == R.RWTTT_E_INVALID
+    assert R.rwttt_version(ctx, 3) == (0, False)
     empty = R.make_group(R.RWTTT_READ, 0, 0)
     assert R.rwttt_read(ctx, empty, R.u32_array([]), 0, 0x1000, 0x2000) == R.RWTTT_OK
     # bad layer, alias inside a group
@@ -185,6 +187,8 @@ def test_fork_checkpoint_resume_validation():
     assert R.rwttt_fork(ctx, 1, 3) == R.RWTTT_E_INVALID
     assert R.rwttt_checkpoint(ctx, 9, [0x5000, 0x6000])[0] == R.RWTTT_E_INVALID
     assert R.rwttt_checkpoint(ctx, 1, [0x5000, 0])[0] == R.RWTTT_E_INVALID
+    assert R.rwttt_checkpoint(ctx, 1, [0x5000, 0x6000])[0] == R.RWTTT_E_INVALID
+    assert R.rwttt_resume(ctx, 1, [0x5000, 0x6000], 3) == R.RWTTT_E_INVALID
     assert R.rwttt_resume(ctx, 1, [0, 0x6000], 3) == R.RWTTT_E_INVALID
     assert R.rwttt_version(ctx, 1) == (0, False)
     assert R.rwttt_rollback(ctx, [2]) == R.RWTTT_OK
