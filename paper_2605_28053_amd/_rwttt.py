@@ -62,6 +62,15 @@ def _load():
         raise ImportError(
             f"{_LIB_PATH} is missing: build the HIP library first "
             "(python -m paper_2605_28053_amd.build)")
+    # One HIP runtime per process: PyTorch-ROCm ships its own libamdhip64 under
+    # the same soname as the system one.  Loading torch first makes the library
+    # bind to torch's runtime, so device memory and streams from torch are
+    # valid here; loaded the other way round the process would hold two
+    # runtimes and the second one finds no device.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = C.CDLL(_LIB_PATH)
     P, U32, U64, I32, VP = C.POINTER, C.c_uint32, C.c_uint64, C.c_int32, C.c_void_p
     sig = {
