@@ -92,7 +92,7 @@ class LaunchTimer:
             return self._streams[handle]
         return self.torch.cuda.current_stream()
 
-    def summary(self, wl):
+    def summary(self, wl, rank=0):
         K, N = wl.d_ff, wl.d_model
         io, st = wl.io_bytes, (4 if wl.state_dtype == "f32" else 2)
         out = {}
@@ -101,7 +101,17 @@ class LaunchTimer:
             if not recs:
                 continue
             ms = sum(s.elapsed_time(e) for _, _, _, s, e in recs)
-            if kind == "read":
+            if rank:
+                # adapter: W0 once, each owner's A and B, x and y; WRITE reads the live
+                # factors, writes the shadow and reads Z and G
+                tok = kind != "write"
+                rb = sum(K * N * io + b * (K + N) * (rank * st + io) for _, b, _, _, _ in recs)
+                rf = sum(b * (2.0 * K * N + 2.0 * rank * (K + N)) for _, b, _, _, _ in recs)
+                wb = sum(b * (2 * (K + N) * rank * st + io * c * (K + N)) for _, b, c, _, _ in recs)
+                wf = sum(4.0 * b * c * rank * (K + N) for _, b, c, _, _ in recs)
+                byt = (rb if tok else 0) + (wb if kind != "read" else 0)
+                flop = (rf if tok else 0) + (wf if kind != "read" else 0)
+            elif kind == "read":
                 byt = sum(K * N * (io + b * st) + b * io * (K + N) for _, b, _, _, _ in recs)
                 flop = sum(4.0 * b * K * N for _, b, _, _, _ in recs)
             else:
@@ -117,7 +127,7 @@ class LaunchTimer:
         return out
 
 
-def prepare(wl, layers, n_steps, threads, keep_layers):
+def prepare(wl, layers, n_steps, threads, keep_layers, rank=0):
     """Device-resident state and inputs for steps [0, n_steps)."""
     import torch
     from rwttt_inputs import TensorSource, WRITE
@@ -125,7 +135,15 @@ def prepare(wl, layers, n_steps, threads, keep_layers):
     from paper_2605_28053_amd.serving import Session, to_device
 
     src = TensorSource(wl, cache_steps=False)
-    sess = Session(wl, None, layers, init_state=False, init_w0=False)
+    backend = 1 if rank else 0
+    sess = Session(wl, None, layers, init_state=False, init_w0=False, backend=backend, rank=rank)
+
+    def init(j):
+        if not rank:
+            return src.dw_init(j[0], j[2])
+        a, b = src.adapter_init(j[0], j[2], rank)
+        return np.concatenate([a.reshape(-1), b.reshape(-1)])
+
     kept = {}
     with ThreadPoolExecutor(threads) as ex:
         for i, arr in enumerate(ex.map(src.w0, layers)):
@@ -133,11 +151,11 @@ def prepare(wl, layers, n_steps, threads, keep_layers):
         jobs = [(r, i, l) for r in range(wl.n_owners) for i, l in enumerate(layers)]
         for lo in range(0, len(jobs), 2 * threads):
             part = jobs[lo:lo + 2 * threads]
-            for (r, i, l), arr in zip(part, ex.map(lambda j: src.dw_init(j[0], j[2]), part)):
+            for (r, i, l), arr in zip(part, ex.map(init, part)):
                 to_device(arr, wl.state_dtype, out=sess.slots[r][i][0])
                 if l in keep_layers:
                     kept[(r, l)] = arr
-        log(f"state resident: {len(jobs)} slots of {wl.state_bytes / 1e6:.1f} MB")
+        log(f"state resident: {len(jobs)} slots of {sess.slots[0][0][0].numel() * sess.slots[0][0][0].element_size() / 1e6:.2f} MB")
 
         L, Rn = len(layers), wl.n_owners
         X = torch.empty((n_steps, L, Rn, wl.d_ff), dtype=torch.bfloat16, device="cuda")
@@ -172,7 +190,7 @@ def run_gpu(args, wl, layers):
     n = args.warmup + args.steps
     t0 = time.time()
     keep = set(args.cpu_layers) if args.cpu_baseline == "on" else set()
-    sess, X, Y, ZG, kept = prepare(wl, layers, n, args.threads, keep)
+    sess, X, Y, ZG, kept = prepare(wl, layers, n, args.threads, keep, args.rank)
     log(f"setup {time.time() - t0:.1f} s")
     from paper_2605_28053_amd.serving import StreamPair
     if args.streams == 2:
@@ -204,7 +222,7 @@ def run_gpu(args, wl, layers):
         writes += len(res.committed) + len(res.rolled_back)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
-    kern = timer.summary(wl) if timer is not None else {}
+    kern = timer.summary(wl, args.rank) if timer is not None else {}
     versions = sess.versions()
     sess.close()
     return dict(tokens=tokens, elapsed=elapsed, kernels=kern, versions=versions,
@@ -225,15 +243,19 @@ def run_cpu_baseline(args, wl, kept):
     steps = range(args.cpu_steps)
     trace = build_trace(wl, args.cpu_steps)
     src = TensorSource(wl)
-    table = O.OwnerTable(wl.n_owners, layers)
-    for r in range(wl.n_owners):
-        for l in layers:
-            arr = kept.get((r, l))
-            table.D[(r, l)] = O.widen(arr if arr is not None else src.dw_init(r, l), wl.state_dtype)
+    table = None
+    if not args.rank:
+        table = O.OwnerTable(wl.n_owners, layers)
+        for r in range(wl.n_owners):
+            for l in layers:
+                arr = kept.get((r, l))
+                table.D[(r, l)] = O.widen(arr if arr is not None else src.dw_init(r, l),
+                                          wl.state_dtype)
     for t in steps:                       # draw the inputs outside the timed window
         src.x_step(t)
     t0 = time.perf_counter()
-    records, _ = O.run_trace(wl, trace, src, steps=steps, layers=layers, table=table)
+    records, _ = O.run_trace(wl, trace, src, steps=steps, layers=layers, table=table,
+                             rank=args.rank)
     dt = time.perf_counter() - t0
     tokens = sum(len(rec.y) for rec in records) / len(layers)
     scale = wl.n_layers / len(layers)
@@ -256,6 +278,8 @@ def main():
     ap.add_argument("--kernel-events", choices=["on", "off"], default="on")
     ap.add_argument("--streams", type=int, choices=[1, 2], default=1,
                     help="2: READ and WRITE groups on two streams, joined every step")
+    ap.add_argument("--rank", type=int, default=0,
+                    help="0: fast-weight state (default); r > 0: the rank-r adapter backend")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run 5 plain device copies of BYTES each (HBM counter calibration)")
     args = ap.parse_args()
@@ -302,8 +326,10 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{wl.name}: 8 streams, {len(layers)} fast-weight layers, d_model "
-                        f"{wl.d_model}, d_ff {wl.d_ff}, bf16 io, fp32 state, 64 READ steps then "
-                        f"one C=64 WRITE per stream, phases staggered by 8",
+                        f"{wl.d_model}, d_ff {wl.d_ff}, bf16 io, fp32 state"
+                        + (f" as rank-{args.rank} adapters (A, B)" if args.rank else "")
+                        + ", 64 READ steps then one C=64 WRITE per stream, phases staggered by 8",
+            "backend": f"delta_adapter rank {args.rank}" if args.rank else "fast_weight",
             "owners": wl.n_owners, "layers": len(layers), "d_model": wl.d_model, "d_ff": wl.d_ff,
             "io": wl.io_dtype, "state": wl.state_dtype, "accumulate": "f32",
             "write_chunk": wl.chunk, "tokens_timed": g["tokens"], "writes_timed": g["writes"],
@@ -313,8 +339,10 @@ def main():
     }
     if "read" in kern:
         rd = kern["read"]
-        traffic = measured_traffic(rd["records"])
-        line["roofline"] = {"bound": "hbm", "kernel": "read_partial_kernel+read_reduce_kernel",
+        traffic = None if args.rank else measured_traffic(rd["records"])
+        line["roofline"] = {"bound": "hbm",
+                            "kernel": ("adapter_read_partial_kernel+adapter_read_reduce_kernel"
+                                       if args.rank else "read_partial_kernel+read_reduce_kernel"),
                             "achieved": round(rd["gbs"], 1), "peak": HBM_PEAK_GBS,
                             "unit": "GB/s", "frac": round(rd["gbs"] / HBM_PEAK_GBS, 4),
                             "traffic": None if traffic is None else round(traffic),
@@ -324,8 +352,11 @@ def main():
     wkind = "write_token" if "write_token" in kern else "write"
     if wkind in kern:
         wr = kern[wkind]
-        line["write_kernel"] = {"kernel": ("write_stream_kernel+read_reduce_kernel (token fused)"
-                                           if wkind == "write_token" else "write update"),
+        wname = ("write_stream_kernel+read_reduce_kernel (token fused)" if wkind == "write_token"
+                 else "write update")
+        if args.rank:
+            wname = "adapter token read + adapter_pq_kernel + adapter_update_kernel"
+        line["write_kernel"] = {"kernel": wname,
                                 "achieved_gbs": round(wr["gbs"], 1),
                                 "hbm_frac": round(wr["gbs"] / HBM_PEAK_GBS, 4),
                                 "achieved_tflops": round(wr["tflops"], 2),

@@ -61,6 +61,12 @@ typedef int32_t rwttt_status;
 /* largest owner group one rwttt_read / rwttt_write call accepts */
 #define RWTTT_MAX_GROUP 64
 
+/* backend types tau (Section 4.1 payloads; Section 4.4 backend instantiations) */
+#define RWTTT_FAST_WEIGHT    0   /* FastWeightState: dW [d_ff, d_model] per (owner, layer)   */
+#define RWTTT_DELTA_ADAPTER  1   /* DeltaAdapterState: low-rank A [d_ff, r], B [r, d_model]   */
+#define RWTTT_MAX_RANK      32   /* largest adapter rank r                                     */
+#define RWTTT_ADAPTER_MAX_CHUNK 1024   /* largest WRITE chunk C of the adapter backend        */
+
 typedef struct rwttt_ctx rwttt_ctx;
 
 /* One ready transition e_i = (r_i, tau_i, sigma_i, rho_i, v_i) plus its ready
@@ -96,11 +102,17 @@ typedef struct rwttt_config {
     int32_t  io_dtype;          /* RWTTT_F32 / RWTTT_BF16: x, W0, y, Z, G         */
     int32_t  state_dtype;       /* RWTTT_F32 / RWTTT_BF16: fast-weight slots      */
     uint32_t max_group;         /* largest group a call accepts, 1..RWTTT_MAX_GROUP */
+    uint32_t backend;           /* RWTTT_FAST_WEIGHT or RWTTT_DELTA_ADAPTER       */
+    uint32_t rank;              /* adapter rank r, 1..RWTTT_MAX_RANK, for
+                                   RWTTT_DELTA_ADAPTER; must be 0 otherwise       */
     uint32_t reserved;          /* must be 0                                      */
     const void* const* w0;      /* [n_layers] device pointers to W0_l             */
     void* const* slots;         /* [n_owners*n_layers*2] device pointers; entry
                                    (owner*n_layers + layer)*2 + s is slot s.
-                                   Slot 0 holds version 0 and starts live.       */
+                                   Slot 0 holds version 0 and starts live.
+                                   A fast-weight slot is dW [d_ff, d_model]; an
+                                   adapter slot is A [d_ff, r] followed by
+                                   B [r, d_model] (rwttt_slot_bytes).            */
     void* workspace;            /* device buffer of rwttt_workspace_bytes() bytes,
                                    or NULL for a host-only context (planning and
                                    the owner table): every call that would touch
@@ -112,9 +124,16 @@ typedef struct rwttt_config {
 /* Bytes of device workspace a context with this config needs: the READ
  * split-K partial sums, n_owners x ceil(d_ff/256) x d_model fp32 values
  * (d_model rounded up to the column tile), and the fused WRITE token's
- * partial sums, n_owners x 48 x d_model fp32 values; one region per owner.
- * Only the shape fields are read.  The workspace needs no initialisation. */
+ * partial sums, n_owners x 48 x d_model fp32 values; for the adapter backend
+ * also n_owners x ceil(d_ff/256) x r partial sums of x A and two
+ * n_owners x RWTTT_ADAPTER_MAX_CHUNK x r scratch matrices of a WRITE; one
+ * region per owner.  Only the shape fields are read.  The workspace needs no
+ * initialisation. */
 rwttt_status rwttt_workspace_bytes(const rwttt_config* cfg, size_t* bytes);
+
+/* Bytes of one state slot: d_ff * d_model (fast weights) or
+ * (d_ff + d_model) * r (adapter) elements of the state dtype. */
+rwttt_status rwttt_slot_bytes(const rwttt_config* cfg, size_t* bytes);
 
 /* Create a context: copies the pointer tables, sets V(r) = 0, slot 0 live and
  * no candidate for every owner.  Makes no HIP call.  Slot pointers must be
@@ -149,7 +168,8 @@ rwttt_status rwttt_plan(const rwttt_ctx* ctx, const rwttt_event* ev, uint32_t n_
 
 /* READ / ApplyState (Section 3, Read; Section 4.2 primitives table): for each
  * slot b of the group, owner r = owner_map[first+b]:
- *     y[r, :] = x[r, :] W0_layer + x[r, :] dW_{r,layer}^live
+ *     y[r, :] = x[r, :] W0_layer + x[r, :] dW_{r,layer}^live          (fast weights)
+ *     y[r, :] = x[r, :] W0_layer + (x[r, :] A_{r,layer}) B_{r,layer}   (adapter)
  * accumulated in fp32 and rounded once to the io dtype.  Versions and slots
  * are unchanged.  Also emits the token of a WRITE step, read at version v
  * before its candidate is committed (Section 3, Write returns y; Section 4.1,
@@ -194,7 +214,11 @@ rwttt_status rwttt_read_append(rwttt_ctx* ctx, const rwttt_group* group, const u
  *     shadow_{r,layer} = live_{r,layer} + eta * Z_b^T G_b
  * with Z_b = z[b] ([chunk, d_ff]) and G_b = g[b] ([chunk, d_model]); the
  * product accumulates in fp32 and the result is rounded once to the state
- * dtype.  `z` and `g` are host arrays of group.count device pointers.  The
+ * dtype.  The adapter backend applies the same evidence to its factors, both
+ * from the live (A, B):
+ *     A' = A + eta * Z^T (G B^T),   B' = B + eta * (Z A)^T G
+ * (the step that moves A B along Z^T G to first order), with
+ * chunk <= RWTTT_ADAPTER_MAX_CHUNK.  `z` and `g` are host arrays of group.count device pointers.  The
  * group must have effect RWTTT_WRITE.
  *
  * A WRITE transition also returns the step's output (Section 3: Write_theta

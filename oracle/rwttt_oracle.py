@@ -118,6 +118,24 @@ def write_candidate(D, Z, G, eta):
     return D + eta * (Z.T @ G)
 
 
+def adapter_read(x, W0, A, B):
+    """y = x W0 + (x A) B for one owner of the DeltaAdapterState backend
+    (Section 4.4; Appendix D).  A: [d_ff, r]; B: [r, d_model]; float64."""
+    return x @ W0 + (x @ A) @ B
+
+
+def adapter_write(A, B, Z, G, eta):
+    """Candidate (A', B') of an adapter WRITE with evidence Z [C, d_ff], G [C, d_model].
+
+    The fast-weight rule moves dW by eta Z^T G.  For dW = A B the same evidence
+    moves each factor along the matching direction, both taken from the live
+    factors: A' = A + eta (Z^T G) B^T = A + eta Z^T (G B^T) and
+    B' = B + eta A^T (Z^T G) = B + eta (Z A)^T G.  Unrounded float64.
+    """
+    M = Z.T @ G
+    return A + eta * (M @ B.T), B + eta * (A.T @ M)
+
+
 # --------------------------------------------------------------------------
 # Planner (Section 3 eqs. event, compatibility, wait-budget; Section 4.3)
 # --------------------------------------------------------------------------
@@ -213,6 +231,11 @@ def plan(events, V, dirty, n_owners, step, B=0, w=0):
 # Owner state table and the serving loop (Algorithm 1)
 # --------------------------------------------------------------------------
 
+def _copy_state(v):
+    """A fast-weight array or an adapter (A, B) pair, copied."""
+    return tuple(a.copy() for a in v) if isinstance(v, tuple) else v.copy()
+
+
 class OwnerTable:
     """Committed fast weights, versions and pending candidates per owner.
 
@@ -255,13 +278,13 @@ class OwnerTable:
         if self.dirty[dst]:
             return E_DIRTY
         for l in self.layers:
-            self.D[(dst, l)] = self.D[(src, l)].copy()
+            self.D[(dst, l)] = _copy_state(self.D[(src, l)])
         self.V[dst] = self.V[src]
         return OK
 
     def checkpoint(self, r):
         """Owner r's committed state and version (the snapshot of Section 4.1)."""
-        return {l: self.D[(r, l)].copy() for l in self.layers}, self.V[r]
+        return {l: _copy_state(self.D[(r, l)]) for l in self.layers}, self.V[r]
 
     def resume(self, r, snap):
         """Restore a checkpoint taken by checkpoint() into owner r."""
@@ -269,7 +292,7 @@ class OwnerTable:
             return E_DIRTY
         state, v = snap
         for l in self.layers:
-            self.D[(r, l)] = state[l].copy()
+            self.D[(r, l)] = _copy_state(state[l])
         self.V[r] = v
         return OK
 
@@ -283,25 +306,35 @@ class StepRecord:
 
 
 def run_trace(wl, trace, src, steps=None, layers=None, cols=None,
-              B=0, w=0, sigma=None, keep_y=True, table=None, on_step=None):
+              B=0, w=0, sigma=None, keep_y=True, table=None, on_step=None, rank=0):
     """Sequential semantics of a workload trace, one owner at a time.
 
     ``cols`` restricts every d_model-indexed tensor (W0, dW, G, y) to a column
     subset.  Both the READ output and the WRITE update of column n only involve
     column n of W0, dW and G, so the restricted run computes exactly those
     columns of the full run.
+
+    ``rank`` > 0 runs the DeltaAdapterState backend instead: each state is the
+    pair (A, B) of that rank, read with adapter_read and updated with
+    adapter_write (no column restriction: an adapter update mixes columns).
     """
     from rwttt_inputs import shape_class
     steps = range(len(trace)) if steps is None else steps
     layers = list(range(wl.n_layers)) if layers is None else list(layers)
     sigma = shape_class if sigma is None else sigma
+    if rank and cols is not None:
+        raise ValueError("an adapter run has no column restriction")
     sel = (lambda a: a) if cols is None else (lambda a: a[..., cols])
 
     if table is None:
         table = OwnerTable(wl.n_owners, layers)
         for r in range(wl.n_owners):
             for l in layers:
-                table.D[(r, l)] = sel(widen(src.dw_init(r, l), wl.state_dtype))
+                if rank:
+                    a, b = src.adapter_init(r, l, rank)
+                    table.D[(r, l)] = (widen(a, wl.state_dtype), widen(b, wl.state_dtype))
+                else:
+                    table.D[(r, l)] = sel(widen(src.dw_init(r, l), wl.state_dtype))
     W0 = {l: sel(widen(src.w0(l), wl.io_dtype)) for l in layers}
 
     records = []
@@ -321,12 +354,17 @@ def run_trace(wl, trace, src, steps=None, layers=None, cols=None,
                     D = table.D[(r, l)]
                     if it.emit:
                         x = widen(src.x(t, r, l), wl.io_dtype)
-                        ys[(r, l)] = round_to(read_apply(x, W0[l], D), wl.io_dtype)
+                        y = adapter_read(x, W0[l], *D) if rank else read_apply(x, W0[l], D)
+                        ys[(r, l)] = round_to(y, wl.io_dtype)
                     if g.effect == WRITE:
                         Z, G = src.zg(t, r, l, it.chunk)
-                        table.cand[(r, l)] = round_to(
-                            write_candidate(D, widen(Z, wl.io_dtype), sel(widen(G, wl.io_dtype)), wl.eta),
-                            wl.state_dtype)
+                        Z, G = widen(Z, wl.io_dtype), sel(widen(G, wl.io_dtype))
+                        if rank:
+                            table.cand[(r, l)] = tuple(round_to(v, wl.state_dtype)
+                                                       for v in adapter_write(*D, Z, G, wl.eta))
+                        else:
+                            table.cand[(r, l)] = round_to(write_candidate(D, Z, G, wl.eta),
+                                                          wl.state_dtype)
             if g.effect == WRITE:
                 for r in g.owners:
                     if by_owner[r].fail:

@@ -27,6 +27,10 @@ RWTTT_WRITE = 1
 RWTTT_F32 = 0
 RWTTT_BF16 = 1
 RWTTT_MAX_GROUP = 64
+RWTTT_FAST_WEIGHT = 0
+RWTTT_DELTA_ADAPTER = 1
+RWTTT_MAX_RANK = 32
+RWTTT_ADAPTER_MAX_CHUNK = 1024
 
 
 class rwttt_event(C.Structure):
@@ -46,7 +50,8 @@ class rwttt_config(C.Structure):
     _fields_ = [("n_owners", C.c_uint32), ("n_layers", C.c_uint32),
                 ("d_ff", C.c_uint32), ("d_model", C.c_uint32),
                 ("io_dtype", C.c_int32), ("state_dtype", C.c_int32),
-                ("max_group", C.c_uint32), ("reserved", C.c_uint32),
+                ("max_group", C.c_uint32), ("backend", C.c_uint32),
+                ("rank", C.c_uint32), ("reserved", C.c_uint32),
                 ("w0", C.POINTER(C.c_void_p)), ("slots", C.POINTER(C.c_void_p)),
                 ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t)]
 
@@ -75,6 +80,7 @@ def _load():
     P, U32, U64, I32, VP = C.POINTER, C.c_uint32, C.c_uint64, C.c_int32, C.c_void_p
     sig = {
         "rwttt_workspace_bytes": (I32, [P(rwttt_config), P(C.c_size_t)]),
+        "rwttt_slot_bytes": (I32, [P(rwttt_config), P(C.c_size_t)]),
         "rwttt_create": (I32, [P(rwttt_config), P(VP)]),
         "rwttt_destroy": (I32, [VP]),
         "rwttt_plan": (I32, [VP, P(rwttt_event), U32, U64, U32, U32,
@@ -126,11 +132,12 @@ def _u32(seq):
 # ---------------------------------------------------------------------------
 
 def make_config(n_owners, n_layers, d_ff, d_model, io_dtype, state_dtype, max_group,
-                w0_ptrs, slot_ptrs, workspace=0, workspace_bytes=0):
+                w0_ptrs, slot_ptrs, workspace=0, workspace_bytes=0, backend=0, rank=0):
     """A ``rwttt_config`` plus the pointer arrays it references (kept alive)."""
     w0 = (C.c_void_p * len(w0_ptrs))(*[int(p) for p in w0_ptrs])
     slots = (C.c_void_p * len(slot_ptrs))(*[int(p) for p in slot_ptrs])
-    cfg = rwttt_config(n_owners, n_layers, d_ff, d_model, io_dtype, state_dtype, max_group, 0,
+    cfg = rwttt_config(n_owners, n_layers, d_ff, d_model, io_dtype, state_dtype, max_group,
+                       backend, rank, 0,
                        C.cast(w0, C.POINTER(C.c_void_p)), C.cast(slots, C.POINTER(C.c_void_p)),
                        int(workspace) or None, int(workspace_bytes))
     cfg._keep = (w0, slots)
@@ -142,6 +149,14 @@ def rwttt_workspace_bytes(cfg):
     st = _lib.rwttt_workspace_bytes(C.byref(cfg), C.byref(out))
     if st != RWTTT_OK:
         raise RwtttError(st, "rwttt_workspace_bytes")
+    return out.value
+
+
+def rwttt_slot_bytes(cfg):
+    out = C.c_size_t(0)
+    st = _lib.rwttt_slot_bytes(C.byref(cfg), C.byref(out))
+    if st != RWTTT_OK:
+        raise RwtttError(st, "rwttt_slot_bytes")
     return out.value
 
 

@@ -38,13 +38,16 @@ def build(verbose=False):
     objdir = os.path.join(PKG, "_build")
     os.makedirs(objdir, exist_ok=True)
     k_obj = os.path.join(objdir, "rwttt_kernels.o")
+    d_obj = os.path.join(objdir, "rwttt_adapter.o")
     a_obj = os.path.join(objdir, "rwttt_api.o")
     _run([HIPCC, "-c", f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS,
           os.path.join(CSRC, "rwttt_kernels.hip"), "-o", k_obj])
     _run([HIPCC, "-c", f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS,
+          os.path.join(CSRC, "rwttt_adapter.hip"), "-o", d_obj])
+    _run([HIPCC, "-c", f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS,
           os.path.join(CSRC, "rwttt_api.cpp"), "-o", a_obj])
     tmp = LIB + ".tmp"
-    _run([HIPCC, "-shared", f"--offload-arch={ARCH}", "-fPIC", a_obj, k_obj, "-o", tmp])
+    _run([HIPCC, "-shared", f"--offload-arch={ARCH}", "-fPIC", a_obj, k_obj, d_obj, "-o", tmp])
     os.replace(tmp, LIB)
     if verbose:
         print("built", LIB)

@@ -26,7 +26,6 @@ struct rwttt_ctx {
   uint32_t epoch = 0;
   uint32_t inject_failures = 0;
   int32_t last_hip = 0;
-  rwttt::ReadGeometry geo{};
 
   size_t li(uint32_t owner, uint32_t layer) const { return size_t(owner) * cfg.n_layers + layer; }
   size_t io_bytes() const { return cfg.io_dtype == RWTTT_BF16 ? 2 : 4; }
@@ -77,7 +76,32 @@ rwttt_status check_shape(const rwttt_config* c) {
   if (!valid_dtype(c->io_dtype) || !valid_dtype(c->state_dtype)) return RWTTT_E_INVALID;
   if (c->max_group == 0 || c->max_group > RWTTT_MAX_GROUP) return RWTTT_E_INVALID;
   if (c->reserved != 0) return RWTTT_E_INVALID;
+  if (c->backend == RWTTT_FAST_WEIGHT) {
+    if (c->rank != 0) return RWTTT_E_INVALID;
+  } else if (c->backend == RWTTT_DELTA_ADAPTER) {
+    if (c->rank == 0 || c->rank > RWTTT_MAX_RANK) return RWTTT_E_INVALID;
+  } else {
+    return RWTTT_E_INVALID;
+  }
   return RWTTT_OK;
+}
+
+bool is_adapter(const rwttt_config* c) { return c->backend == RWTTT_DELTA_ADAPTER; }
+
+size_t slot_bytes_of(const rwttt_config* c) {
+  const size_t s = c->state_dtype == RWTTT_BF16 ? 2 : 4;
+  if (is_adapter(c)) return (size_t(c->d_ff) + c->d_model) * c->rank * s;
+  return size_t(c->d_ff) * c->d_model * s;
+}
+
+size_t workspace_bytes_of(const rwttt_config* c) {
+  if (is_adapter(c))
+    return rwttt::adapter_geometry(int(c->d_ff), int(c->d_model), c->io_dtype == RWTTT_BF16,
+                                   int(c->rank), int(c->n_owners))
+        .total_bytes;
+  return rwttt::read_geometry(int(c->d_ff), int(c->d_model), c->state_dtype == RWTTT_BF16,
+                              int(c->n_owners))
+      .total_bytes;
 }
 
 rwttt_status hip_fail(rwttt_ctx* ctx, hipError_t e) {
@@ -93,9 +117,15 @@ rwttt_status rwttt_workspace_bytes(const rwttt_config* cfg, size_t* bytes) {
   const rwttt_status s = check_shape(cfg);
   if (s != RWTTT_OK) return s;
   if (!bytes) return RWTTT_E_INVALID;
-  *bytes = rwttt::read_geometry(int(cfg->d_ff), int(cfg->d_model), cfg->state_dtype == RWTTT_BF16,
-                                int(cfg->n_owners))
-               .total_bytes;
+  *bytes = workspace_bytes_of(cfg);
+  return RWTTT_OK;
+}
+
+rwttt_status rwttt_slot_bytes(const rwttt_config* cfg, size_t* bytes) {
+  const rwttt_status s = check_shape(cfg);
+  if (s != RWTTT_OK) return s;
+  if (!bytes) return RWTTT_E_INVALID;
+  *bytes = slot_bytes_of(cfg);
   return RWTTT_OK;
 }
 
@@ -111,11 +141,9 @@ rwttt_status rwttt_create(const rwttt_config* cfg, rwttt_ctx** out) {
     if (!p || !aligned16(p)) return RWTTT_E_INVALID;
   std::sort(sorted.begin(), sorted.end());
   if (std::adjacent_find(sorted.begin(), sorted.end()) != sorted.end()) return RWTTT_E_OWNER_ALIAS;
-  const rwttt::ReadGeometry geo = rwttt::read_geometry(
-      int(cfg->d_ff), int(cfg->d_model), cfg->state_dtype == RWTTT_BF16, int(cfg->n_owners));
   if (cfg->workspace) {
     if ((reinterpret_cast<uintptr_t>(cfg->workspace) & 255u) != 0) return RWTTT_E_INVALID;
-    if (cfg->workspace_bytes < geo.total_bytes) return RWTTT_E_CAPACITY;
+    if (cfg->workspace_bytes < workspace_bytes_of(cfg)) return RWTTT_E_CAPACITY;
   }
 
   rwttt_ctx* ctx = new (std::nothrow) rwttt_ctx;
@@ -123,7 +151,6 @@ rwttt_status rwttt_create(const rwttt_config* cfg, rwttt_ctx** out) {
   ctx->cfg = *cfg;
   ctx->cfg.w0 = nullptr;
   ctx->cfg.slots = nullptr;
-  ctx->geo = geo;
   ctx->w0.assign(cfg->w0, cfg->w0 + cfg->n_layers);
   ctx->slots.assign(cfg->slots, cfg->slots + n_slots);
   const size_t nl = size_t(cfg->n_owners) * cfg->n_layers;
@@ -275,6 +302,32 @@ rwttt_status read_impl(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t*
       if (ctx->tail_len[ctx->li(owners[b], layer)] >= ctx->tail_rows) return RWTTT_E_CAPACITY;
   }
 
+  if (is_adapter(&ctx->cfg)) {
+    rwttt::AdapterReadLaunch A;
+    A.io_bf16 = ctx->cfg.io_dtype == RWTTT_BF16;
+    A.state_bf16 = ctx->cfg.state_dtype == RWTTT_BF16;
+    A.d_ff = int(ctx->cfg.d_ff);
+    A.d_model = int(ctx->cfg.d_model);
+    A.rank = int(ctx->cfg.rank);
+    A.count = int(n);
+    A.n_owners = int(ctx->cfg.n_owners);
+    A.x = x;
+    A.y = y;
+    A.w0 = ctx->w0[layer];
+    A.workspace = ctx->cfg.workspace;
+    for (uint32_t b = 0; b < n; ++b) {
+      const uint32_t r = owners[b];
+      A.state[b] = ctx->slot(r, layer, 0);
+      A.row[b] = r;
+      A.tail[b] = append ? ctx->tail_row(r, layer, ctx->tail_len[ctx->li(r, layer)]) : nullptr;
+    }
+    const hipError_t e = rwttt::launch_adapter_read(A, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(ctx, e);
+    if (append)
+      for (uint32_t b = 0; b < n; ++b) ++ctx->tail_len[ctx->li(owners[b], layer)];
+    return RWTTT_OK;
+  }
+
   rwttt::ReadLaunch L;
   L.io_bf16 = ctx->cfg.io_dtype == RWTTT_BF16;
   L.state_bf16 = ctx->cfg.state_dtype == RWTTT_BF16;
@@ -341,6 +394,7 @@ rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_
   if (from_tail && (ctx->tail.empty() || !x || chunk > ctx->tail_rows)) return RWTTT_E_INVALID;
   if (x && (!ctx->cfg.workspace || !aligned16(x) || !aligned16(y))) return RWTTT_E_INVALID;
   if (chunk > (1u << 20)) return RWTTT_E_INVALID;
+  if (is_adapter(&ctx->cfg) && chunk > RWTTT_ADAPTER_MAX_CHUNK) return RWTTT_E_INVALID;
   if (n > ctx->cfg.max_group) return RWTTT_E_CAPACITY;
   const uint32_t* owners = owner_map + group->first;
   rwttt_status why = RWTTT_OK;
@@ -404,7 +458,52 @@ rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_
     if (e == hipSuccess)
       for (uint32_t b = 0; b < n; ++b) ctx->tail_len[ctx->li(owners[b], layer)] = chunk;
   }
-  if (e == hipSuccess) e = rwttt::launch_write(L, static_cast<hipStream_t>(stream));
+  if (e == hipSuccess && is_adapter(&ctx->cfg)) {
+    if (x) {
+      // the step's token at version v, then the factor update
+      rwttt::AdapterReadLaunch A;
+      A.io_bf16 = L.io_bf16;
+      A.state_bf16 = L.state_bf16;
+      A.d_ff = L.d_ff;
+      A.d_model = L.d_model;
+      A.rank = int(ctx->cfg.rank);
+      A.count = L.count;
+      A.n_owners = L.n_owners;
+      A.x = x;
+      A.y = y;
+      A.w0 = L.w0;
+      A.workspace = L.workspace;
+      for (uint32_t b = 0; b < n; ++b) {
+        A.state[b] = L.live[b];
+        A.row[b] = owners[b];
+        A.tail[b] = nullptr;
+      }
+      e = rwttt::launch_adapter_read(A, static_cast<hipStream_t>(stream));
+    }
+    if (e == hipSuccess) {
+      rwttt::AdapterWriteLaunch W;
+      W.io_bf16 = L.io_bf16;
+      W.state_bf16 = L.state_bf16;
+      W.d_ff = L.d_ff;
+      W.d_model = L.d_model;
+      W.rank = int(ctx->cfg.rank);
+      W.count = L.count;
+      W.chunk = L.chunk;
+      W.n_owners = L.n_owners;
+      W.eta = eta;
+      W.workspace = L.workspace;
+      for (uint32_t b = 0; b < n; ++b) {
+        W.live[b] = L.live[b];
+        W.shadow[b] = L.shadow[b];
+        W.z[b] = L.z[b];
+        W.g[b] = L.g[b];
+        W.row[b] = owners[b];
+      }
+      e = rwttt::launch_adapter_write(W, static_cast<hipStream_t>(stream));
+    }
+  } else if (e == hipSuccess) {
+    e = rwttt::launch_write(L, static_cast<hipStream_t>(stream));
+  }
   if (e != hipSuccess) {
     for (uint32_t b = 0; b < n; ++b) ctx->failed[owners[b]] = 1;
     return hip_fail(ctx, e);
@@ -457,8 +556,7 @@ rwttt_status rwttt_fork(rwttt_ctx* ctx, uint32_t src, uint32_t dst, void* stream
   if (src == dst) return RWTTT_E_OWNER_ALIAS;
   if (ctx->dirty[dst]) return RWTTT_E_DIRTY;
   if (!ctx->cfg.workspace) return RWTTT_E_INVALID;
-  const size_t state_bytes = size_t(ctx->cfg.d_ff) * ctx->cfg.d_model *
-                             (ctx->cfg.state_dtype == RWTTT_BF16 ? 2 : 4);
+  const size_t state_bytes = slot_bytes_of(&ctx->cfg);
   std::vector<rwttt::CopyJob> jobs;
   for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l) {
     jobs.push_back({ctx->slot(src, l, 0), ctx->slot(dst, l, 0), state_bytes});
@@ -485,8 +583,7 @@ rwttt_status rwttt_checkpoint(rwttt_ctx* ctx, uint32_t owner, void* const* dst, 
   if (!ctx->cfg.workspace) return RWTTT_E_INVALID;   // host-only context: no device copies
   for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l)
     if (!dst[l]) return RWTTT_E_INVALID;
-  const size_t state_bytes = size_t(ctx->cfg.d_ff) * ctx->cfg.d_model *
-                             (ctx->cfg.state_dtype == RWTTT_BF16 ? 2 : 4);
+  const size_t state_bytes = slot_bytes_of(&ctx->cfg);
   for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l) {
     const hipError_t e = hipMemcpyAsync(dst[l], ctx->slot(owner, l, 0), state_bytes,
                                         hipMemcpyDefault, static_cast<hipStream_t>(stream));
@@ -503,8 +600,7 @@ rwttt_status rwttt_resume(rwttt_ctx* ctx, uint32_t owner, const void* const* src
   if (!ctx->cfg.workspace) return RWTTT_E_INVALID;   // host-only context: no device copies
   for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l)
     if (!src[l]) return RWTTT_E_INVALID;
-  const size_t state_bytes = size_t(ctx->cfg.d_ff) * ctx->cfg.d_model *
-                             (ctx->cfg.state_dtype == RWTTT_BF16 ? 2 : 4);
+  const size_t state_bytes = slot_bytes_of(&ctx->cfg);
   for (uint32_t l = 0; l < ctx->cfg.n_layers; ++l) {
     const hipError_t e = hipMemcpyAsync(ctx->slot(owner, l, 0), src[l], state_bytes,
                                         hipMemcpyDefault, static_cast<hipStream_t>(stream));

@@ -71,6 +71,45 @@ struct WriteLaunch {
 hipError_t launch_read(const ReadLaunch& L, hipStream_t stream);
 hipError_t launch_tail_append(const TailLaunch& L, hipStream_t stream);
 
+// ---- DeltaAdapterState backend (rwttt_adapter.hip) ----
+//
+// A slot holds A [d_ff, rank] then B [rank, d_model], row-major, state dtype.
+// The workspace follows the fast-weight layout (its READ partial region is
+// reused for the W0 partial sums, tiled by the io dtype) with the x A partial
+// sums and the WRITE's P = G B^T and Q = Z A behind it.
+struct AdapterGeometry {
+  int ks, nt, npad;          // W0 partial sums: K chunks, column tiles, padded row
+  size_t part_floats;        // n_owners * ks * npad
+  size_t u_offset;           // bytes: x A partials, n_owners * ks * rank floats
+  size_t pq_offset;          // bytes: P then Q, each n_owners * max_chunk * rank floats
+  size_t total_bytes;
+};
+AdapterGeometry adapter_geometry(int d_ff, int d_model, int io_bf16, int rank, int n_owners);
+
+struct AdapterReadLaunch {
+  int io_bf16, state_bf16, d_ff, d_model, rank, count, n_owners;
+  const void* x;
+  void* y;
+  const void* w0;
+  void* workspace;
+  const void* state[RWTTT_MAX_GROUP];   // live slot of each group slot
+  uint32_t row[RWTTT_MAX_GROUP];
+  void* tail[RWTTT_MAX_GROUP];          // tail row receiving x, or null
+};
+hipError_t launch_adapter_read(const AdapterReadLaunch& L, hipStream_t stream);
+
+struct AdapterWriteLaunch {
+  int io_bf16, state_bf16, d_ff, d_model, rank, count, chunk, n_owners;
+  float eta;
+  void* workspace;
+  const void* live[RWTTT_MAX_GROUP];
+  void* shadow[RWTTT_MAX_GROUP];
+  const void* z[RWTTT_MAX_GROUP];
+  const void* g[RWTTT_MAX_GROUP];
+  uint32_t row[RWTTT_MAX_GROUP];
+};
+hipError_t launch_adapter_write(const AdapterWriteLaunch& L, hipStream_t stream);
+
 // Device-to-device copies of n 16-byte-aligned regions (one launch per 64).
 struct CopyJob {
   const void* src;

@@ -86,15 +86,19 @@ class Session:
     """Device-resident state of one workload plus the serving loop."""
 
     def __init__(self, wl, src=None, layers=None, max_group=None, device="cuda",
-                 init_state=True, init_w0=True, tail_rows=None):
+                 init_state=True, init_w0=True, tail_rows=None, backend=R.RWTTT_FAST_WEIGHT,
+                 rank=0):
         self.wl = wl
         self.device = device
+        self.backend, self.rank = backend, rank
         self.layers = list(range(wl.n_layers)) if layers is None else list(layers)
         self.L = len(self.layers)
         sdt, iodt = TORCH_DTYPE[wl.state_dtype], TORCH_DTYPE[wl.io_dtype]
         K, N = wl.d_ff, wl.d_model
+        # a fast-weight slot is dW [K, N]; an adapter slot is A [K, r] then B [r, N]
+        shape = (K, N) if backend == R.RWTTT_FAST_WEIGHT else ((K + N) * rank,)
         self.w0 = [torch.empty((K, N), dtype=iodt, device=device) for _ in self.layers]
-        self.slots = [[[torch.empty((K, N), dtype=sdt, device=device) for _ in range(2)]
+        self.slots = [[[torch.empty(shape, dtype=sdt, device=device) for _ in range(2)]
                        for _ in self.layers] for _ in range(wl.n_owners)]
         if src is not None and init_w0:
             for i, l in enumerate(self.layers):
@@ -102,14 +106,20 @@ class Session:
         if src is not None and init_state:
             for r in range(wl.n_owners):
                 for i, l in enumerate(self.layers):
-                    to_device(src.dw_init(r, l), wl.state_dtype, device, out=self.slots[r][i][0])
+                    if backend == R.RWTTT_FAST_WEIGHT:
+                        to_device(src.dw_init(r, l), wl.state_dtype, device, out=self.slots[r][i][0])
+                    else:
+                        a, b = src.adapter_init(r, l, rank)
+                        to_device(np.concatenate([a.reshape(-1), b.reshape(-1)]), wl.state_dtype,
+                                  device, out=self.slots[r][i][0])
         self.max_group = max_group or min(R.RWTTT_MAX_GROUP, wl.n_owners)
         slot_ptrs = []
         for r in range(wl.n_owners):
             for i in range(self.L):
                 slot_ptrs += [self.slots[r][i][0].data_ptr(), self.slots[r][i][1].data_ptr()]
         cfg = R.make_config(wl.n_owners, self.L, K, N, CODE[wl.io_dtype], CODE[wl.state_dtype],
-                            self.max_group, [w.data_ptr() for w in self.w0], slot_ptrs)
+                            self.max_group, [w.data_ptr() for w in self.w0], slot_ptrs,
+                            backend=backend, rank=rank)
         ws_bytes = R.rwttt_workspace_bytes(cfg)
         self.workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=device)
         cfg.workspace = self.workspace.data_ptr()
@@ -158,12 +168,17 @@ class Session:
         a, b = self.slots[r][li]
         return a if a.data_ptr() == ptr else b
 
+    def factors(self, slot):
+        """(A [d_ff, r], B [r, d_model]) views of an adapter slot tensor."""
+        K, N, r = self.wl.d_ff, self.wl.d_model, self.rank
+        return slot[:K * r].view(K, r), slot[K * r:].view(r, N)
+
     # ---- one decode step (Algorithm 1) ------------------------------------
     def events(self, t, items):
         evs = []
         for it in items:
             v, _ = R.rwttt_version(self.ctx, it.owner)
-            evs.append((it.owner, 0, shape_class(self.wl, it.effect, it.chunk), 0,
+            evs.append((it.owner, self.backend, shape_class(self.wl, it.effect, it.chunk), 0,
                         it.effect, v, t))
         return evs
 

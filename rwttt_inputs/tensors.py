@@ -15,7 +15,7 @@ import numpy as np
 
 from .workloads import Workload
 
-K_W0, K_DW, K_X, K_Z, K_G, K_TEST = 1, 2, 3, 4, 5, 9
+K_W0, K_DW, K_X, K_Z, K_G, K_ADA_A, K_ADA_B, K_TEST = 1, 2, 3, 4, 5, 6, 7, 9
 
 
 def f32_to_bf16_bits(a):
@@ -58,6 +58,7 @@ class TensorSource:
     x(t, r, l)      [d_ff]               io dtype
     w0(l)           [d_ff, d_model]      io dtype
     dw_init(r, l)   [d_ff, d_model]      state dtype (zeros when dw_std == 0)
+    adapter_init(r, l, rank)  ([d_ff, rank], [rank, d_model])  state dtype
     zg(t, r, l, C)  ([C, d_ff], [C, d_model])  io dtype
     """
 
@@ -95,6 +96,16 @@ class TensorSource:
             return np.zeros((wl.d_ff, wl.d_model), dtype=dt)
         return self._remember(("dw", r, l), lambda: draw(
             (wl.d_ff, wl.d_model), wl.dw_std, wl.state_dtype, wl.seed, (K_DW, r, l)))
+
+    def adapter_init(self, r, l, rank):
+        """Initial low-rank factors of the adapter backend, state dtype:
+        A [d_ff, rank] ~ N(0, 1/d_ff), B [rank, d_model] ~ N(0, 1/rank)."""
+        wl = self.wl
+        return self._remember(("ada", r, l, rank), lambda: (
+            draw((wl.d_ff, rank), float(1.0 / np.sqrt(wl.d_ff)), wl.state_dtype, wl.seed,
+                 (K_ADA_A, r, l, rank)),
+            draw((rank, wl.d_model), float(1.0 / np.sqrt(rank)), wl.state_dtype, wl.seed,
+                 (K_ADA_B, r, l, rank))))
 
     # ---- per-step activations --------------------------------------------
     def x_step(self, t):

@@ -525,3 +525,110 @@ def test_fork_checkpoint_resume_are_independent_copies():
     # resume returns the parent to its checkpoint, exactly
     assert table.resume(0, snap) == O.OK
     assert table.V[0] == 2 and np.array_equal(table.D[(0, 0)], child)
+
+
+# --------------------------------------------------------------------------
+# DeltaAdapterState backend (Section 4.4; Appendix D)
+# --------------------------------------------------------------------------
+
+def _adapter_case(K=24, N=16, r=3, C=5, seed=4):
+    rng = np.random.default_rng(seed)
+    return (rng.standard_normal(K), rng.standard_normal((K, N)), rng.standard_normal((K, r)),
+            rng.standard_normal((r, N)), np.abs(rng.standard_normal((C, K))),
+            rng.standard_normal((C, N)))
+
+
+def test_adapter_read_equals_fast_weight_read_of_the_materialised_delta():
+    """Exact apply equivalence: x W0 + (x A) B == x W0 + x (A B)."""
+    x, W0, A, B, _, _ = _adapter_case()
+    got = O.adapter_read(x, W0, A, B)
+    assert np.allclose(got, O.read_apply(x, W0, A @ B), rtol=1e-12, atol=1e-12)
+    K, N = W0.shape
+    brute = [math.fsum([x[k] * W0[k, n] for k in range(K)] +
+                       [x[k] * A[k, j] * B[j, n] for k in range(K) for j in range(A.shape[1])])
+             for n in range(N)]
+    assert np.allclose(got, brute, rtol=1e-12, atol=1e-12)
+
+
+def test_adapter_write_moves_each_factor_along_the_evidence_gradient():
+    """(A' - A) / eta and (B' - B) / eta equal the finite-difference derivatives of
+    <Z^T G, A B> (the quantity the fast-weight rule increases), each factor
+    taken at the live value."""
+    _, _, A, B, Z, G = _adapter_case()
+    eta = 0.37
+    A1, B1 = O.adapter_write(A, B, Z, G, eta)
+    M = Z.T @ G
+
+    def f(a, b):
+        return float(np.sum(M * (a @ b)))
+
+    h = 1e-6
+    for (i, j) in [(0, 0), (7, 2), (23, 1)]:
+        d = np.zeros_like(A)
+        d[i, j] = h
+        fd = (f(A + d, B) - f(A - d, B)) / (2 * h)
+        assert abs((A1[i, j] - A[i, j]) / eta - fd) < 1e-6 * max(1.0, abs(fd))
+    for (i, j) in [(0, 0), (2, 15), (1, 7)]:
+        d = np.zeros_like(B)
+        d[i, j] = h
+        fd = (f(A, B + d) - f(A, B - d)) / (2 * h)
+        assert abs((B1[i, j] - B[i, j]) / eta - fd) < 1e-6 * max(1.0, abs(fd))
+
+
+def test_adapter_write_special_cases():
+    _, _, A, B, Z, G = _adapter_case()
+    eta = 0.1
+    # zero B: A is unchanged and B' = eta (Z A)^T G
+    A1, B1 = O.adapter_write(A, np.zeros_like(B), Z, G, eta)
+    assert np.array_equal(A1, A)
+    assert np.allclose(B1, eta * (Z @ A).T @ G, rtol=1e-12)
+    # zero A: B is unchanged
+    A1, B1 = O.adapter_write(np.zeros_like(A), B, Z, G, eta)
+    assert np.array_equal(B1, B)
+    # one evidence row: A' = A + eta outer(z, B g)
+    A1, B1 = O.adapter_write(A, B, Z[:1], G[:1], eta)
+    assert np.allclose(A1, A + eta * np.outer(Z[0], B @ G[0]), rtol=1e-12)
+    assert np.allclose(B1, B + eta * np.outer(A.T @ Z[0], G[0]), rtol=1e-12)
+    # eta = 0 is the identity
+    A1, B1 = O.adapter_write(A, B, Z, G, 0.0)
+    assert np.array_equal(A1, A) and np.array_equal(B1, B)
+
+
+def test_adapter_write_first_order_moves_the_product_like_the_fast_weight_rule():
+    """A' B' - A B = eta (M B^T B + A A^T M) + O(eta^2), M = Z^T G."""
+    _, _, A, B, Z, G = _adapter_case()
+    M = Z.T @ G
+    lin = M @ B.T @ B + A @ A.T @ M
+    for eta in (1e-4, 1e-5):
+        A1, B1 = O.adapter_write(A, B, Z, G, eta)
+        err = (A1 @ B1 - A @ B) / eta - lin
+        assert np.max(np.abs(err)) <= 50 * eta * np.max(np.abs(M)) ** 2 * max(1.0, np.max(np.abs(A)) * np.max(np.abs(B)))
+
+
+def test_adapter_trace_equals_per_request_sequential_application():
+    """The adapter run plans and versions exactly like the fast-weight run (the
+    plan never looks at the payload), and its outputs equal each request walked
+    alone through adapter_read / adapter_write in order."""
+    wl, rank = workload(0), 3
+    trace, src = build_trace(wl), TensorSource(wl)
+    fw, _ = O.run_trace(wl, trace, src)
+    ad, table = O.run_trace(wl, trace, src, rank=rank)
+    assert [r.versions for r in ad] == [r.versions for r in fw]
+    assert [[(g.key, g.owners) for g in r.plan.groups] for r in ad] == \
+           [[(g.key, g.owners) for g in r.plan.groups] for r in fw]
+    W0 = O.widen(src.w0(0), "f32")
+    for r in range(wl.n_owners):
+        a, b = src.adapter_init(r, 0, rank)
+        A, B = O.widen(a, "f32"), O.widen(b, "f32")
+        for t in range(wl.n_steps):
+            it = next(i for i in trace[t] if i.owner == r)
+            x = O.widen(src.x(t, r, 0), "f32")
+            y = (x @ A) @ B + x @ W0
+            assert O.max_rel_floor(ad[t].y[(r, 0)], y) <= 1e-6
+            if it.effect == WRITE and not it.fail:
+                Z, G = src.zg(t, r, 0, it.chunk)
+                Z, G = O.widen(Z, "f32"), O.widen(G, "f32")
+                A, B = A + wl.eta * (Z.T @ (G @ B.T)), B + wl.eta * ((Z @ A).T @ G)
+                A, B = A.astype(np.float32).astype(np.float64), B.astype(np.float32).astype(np.float64)
+        assert O.rel_frobenius(table.D[(r, 0)][0], A) < 1e-6
+        assert O.rel_frobenius(table.D[(r, 0)][1], B) < 1e-6
