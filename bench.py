@@ -39,6 +39,18 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+KERNEL_SOURCES = ("rwttt_kernels.hip", "rwttt_device.h", "rwttt_kernels.h")
+
+
+def kernel_source_sha():
+    """SHA-256 over the fast-weight kernel sources, in a fixed order."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2605_28053_amd", "csrc", name), "rb").read())
+    return h.hexdigest()
+
+
 def measured_traffic(records):
     """Mean HBM bytes per READ call from the committed rocprofv3 PMC summary.
 
@@ -46,12 +58,10 @@ def measured_traffic(records):
     the same counters read for a plain 1 GiB device copy.  It is used only if
     the kernel source is the one the counters were taken on; else None.
     """
-    import hashlib
     path = os.path.join(ROOT, "profiles", "hbm_traffic__mixed8-4b-36L.json")
-    src = os.path.join(ROOT, "paper_2605_28053_amd", "csrc", "rwttt_kernels.hip")
     try:
         summ = json.load(open(path))
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        sha = kernel_source_sha()
     except OSError:
         return None
     if summ.get("kernel_source_sha256") != sha:

@@ -32,7 +32,8 @@ namespace {
 //    from HBM once and is re-read from that XCD's L2.  dW is streamed with
 //    non-temporal loads so it does not evict W0.  The four waves' sums are
 //    added through LDS in a fixed order into one partial per (owner, chunk).
-// 2. read_reduce_kernel: y[b, n] = sum over chunks, in chunk order.
+// 2. read_reduce_kernel: y[b, n] = sum over chunks: four contiguous quarters
+//    of the chunks, each in chunk order, added in order.
 //
 // Partials are indexed by owner id, so concurrent reads of disjoint owner sets
 // (one per stream) never touch the same workspace bytes.
@@ -126,23 +127,35 @@ __global__ void __launch_bounds__(kReadThreads) read_partial_kernel(const ReadPa
     dst[j] = ((red[0][j] + red[1][j]) + red[2][j]) + red[3][j];
 }
 
+// 64 output columns per block; the four waves each add a contiguous quarter of
+// the chunks in chunk order with all of its loads in flight at once, and the
+// quarters are added in order.
+constexpr int kRedCols = 64;
+constexpr int kRedBatch = 16;
+
 template <typename IO>
 __global__ void __launch_bounds__(256) read_reduce_kernel(const ReadParams p) {
+  __shared__ float qs[4][kRedCols];
   const int b = blockIdx.y;
-  const int n = blockIdx.x * 256 + threadIdx.x;
-  if (n >= p.d_model) return;
-  const float* q = p.part + size_t(p.row[b]) * p.ks * p.npad + n;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = blockIdx.x * kRedCols + lane;
+  const int per = (p.ks + 3) / 4;
+  const int k0 = wave * per, k1 = min(p.ks, k0 + per);
   float s = 0.f;
-  int k = 0;
-  for (; k + 8 <= p.ks; k += 8) {
-    float a[8];
+  if (n < p.d_model) {
+    const float* q = p.part + size_t(p.row[b]) * p.ks * p.npad + n;
+    for (int k = k0; k < k1; k += kRedBatch) {
+      float a[kRedBatch];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) a[u] = q[size_t(k + u) * p.npad];
+      for (int u = 0; u < kRedBatch; ++u) a[u] = k + u < k1 ? q[size_t(k + u) * p.npad] : 0.f;
 #pragma unroll
-    for (int u = 0; u < 8; ++u) s += a[u];
+      for (int u = 0; u < kRedBatch; ++u) s += a[u];
+    }
   }
-  for (; k < p.ks; ++k) s += q[size_t(k) * p.npad];
-  Elem<IO>::put(p.y, size_t(p.row[b]) * p.d_model + n, s);
+  qs[wave][lane] = s;
+  __syncthreads();
+  if (wave == 0 && n < p.d_model)
+    Elem<IO>::put(p.y, size_t(p.row[b]) * p.d_model + n, ((qs[0][lane] + qs[1][lane]) + qs[2][lane]) + qs[3][lane]);
 }
 
 // ---------------------------------------------------------------------------
@@ -674,7 +687,7 @@ hipError_t launch_read_t(const ReadLaunch& L, hipStream_t stream) {
   const unsigned pairs8 = unsigned((g.ks * g.nt + 7) / 8 * 8);
   hipLaunchKernelGGL((read_partial_kernel<IO, ST>), dim3(pairs8 * unsigned(L.count)),
                      dim3(kReadThreads), 0, stream, p);
-  hipLaunchKernelGGL((read_reduce_kernel<IO>), dim3((L.d_model + 255) / 256, L.count), dim3(256),
+  hipLaunchKernelGGL((read_reduce_kernel<IO>), dim3((L.d_model + kRedCols - 1) / kRedCols, L.count), dim3(256),
                      0, stream, p);
   return hipGetLastError();
 }
@@ -729,7 +742,7 @@ hipError_t launch_write_t(const WriteLaunch& L, hipStream_t stream) {
         q.row[b] = b < L.count ? L.row[b] : 0u;
         q.tail[b] = nullptr;
       }
-      hipLaunchKernelGGL((read_reduce_kernel<uint16_t>), dim3((L.d_model + 255) / 256, L.count),
+      hipLaunchKernelGGL((read_reduce_kernel<uint16_t>), dim3((L.d_model + kRedCols - 1) / kRedCols, L.count),
                          dim3(256), 0, stream, q);
     } else {
       hipLaunchKernelGGL((write_stream_kernel<ST, false>), grid, dim3(256), 0, stream, p);
