@@ -137,11 +137,20 @@ class LaunchTimer:
         return out
 
 
+def items_fn(wl):
+    """t -> the step's StepItems; a finite trace is built once."""
+    from rwttt_inputs import build_trace
+    from rwttt_inputs.schedule import step_items
+    if wl.schedule in ("staggered", "read_only"):
+        return lambda t: step_items(wl, t)
+    trace = build_trace(wl)
+    return lambda t: trace[t]
+
+
 def prepare(wl, layers, n_steps, threads, keep_layers, rank=0):
     """Device-resident state and inputs for steps [0, n_steps)."""
     import torch
     from rwttt_inputs import TensorSource, WRITE
-    from rwttt_inputs.schedule import step_items
     from paper_2605_28053_amd.serving import Session, to_device
 
     src = TensorSource(wl, cache_steps=False)
@@ -176,8 +185,9 @@ def prepare(wl, layers, n_steps, threads, keep_layers, rank=0):
 
         for t, arr in enumerate(ex.map(xs, range(n_steps))):
             to_device(arr, wl.io_dtype, out=X[t])
+        items_at = items_fn(wl)
         writes = [(t, it.owner, it.chunk) for t in range(n_steps)
-                  for it in step_items(wl, t) if it.effect == WRITE]
+                  for it in items_at(t) if it.effect == WRITE]
 
         def zg(w):
             Z, G = src.zg_owner(*w)
@@ -195,9 +205,11 @@ def prepare(wl, layers, n_steps, threads, keep_layers, rank=0):
 
 def run_gpu(args, wl, layers):
     import torch
-    from rwttt_inputs.schedule import step_items
 
-    n = args.warmup + args.steps
+    periodic = wl.schedule in ("staggered", "read_only")
+    # a periodic schedule runs warm-up steps then the timed steps; a finite one
+    # (ragged, prefill then decode) runs its whole trace once untimed, then again timed
+    n = args.warmup + args.steps if periodic else wl.n_steps
     t0 = time.time()
     keep = set(args.cpu_layers) if args.cpu_baseline == "on" else set()
     sess, X, Y, ZG, kept = prepare(wl, layers, n, args.threads, keep, args.rank)
@@ -211,14 +223,18 @@ def run_gpu(args, wl, layers):
         sp, tstreams = torch.cuda.current_stream().cuda_stream, ()
     y_ptrs = [Y[i].data_ptr() for i in range(len(layers))]
 
+    items_at = items_fn(wl)
+
     def one(t, timer=None):
-        items = step_items(wl, t)
+        items = items_at(t)
         x_ptrs = [X[t, i].data_ptr() for i in range(len(layers))]
         zg = {r: (ZG[(t, r)][2], ZG[(t, r)][3]) for r in [it.owner for it in items] if (t, r) in ZG}
         res = sess.step(t, items, x_ptrs, y_ptrs, zg, sp, timer=timer)
         return sum(1 for it in items if it.emit), res
 
-    for t in range(args.warmup):
+    warm = range(args.warmup) if periodic else range(n)
+    timed = range(args.warmup, n) if periodic else range(n)
+    for t in warm:
         one(t)
     torch.cuda.synchronize()
     timer = LaunchTimer(torch, tstreams) if args.kernel_events == "on" else None
@@ -226,7 +242,7 @@ def run_gpu(args, wl, layers):
     writes = 0
     torch.cuda.synchronize()
     t_start = time.perf_counter()
-    for t in range(args.warmup, n):
+    for t in timed:
         k, res = one(t, timer)
         tokens += k
         writes += len(res.committed) + len(res.rolled_back)
@@ -236,7 +252,7 @@ def run_gpu(args, wl, layers):
     versions = sess.versions()
     sess.close()
     return dict(tokens=tokens, elapsed=elapsed, kernels=kern, versions=versions,
-                writes=writes, kept=kept)
+                writes=writes, kept=kept, steps=len(timed), warmup=len(warm))
 
 
 def run_cpu_baseline(args, wl, kept):
@@ -249,9 +265,9 @@ def run_cpu_baseline(args, wl, kept):
                             if i.get("user_api") == "blas"] or [1])
     except Exception:
         blas_threads = os.cpu_count()
-    layers = list(args.cpu_layers)
-    steps = range(args.cpu_steps)
-    trace = build_trace(wl, args.cpu_steps)
+    layers = [l for l in args.cpu_layers if l < wl.n_layers] or [0]
+    steps = range(min(args.cpu_steps, wl.n_steps))
+    trace = build_trace(wl, len(steps))
     src = TensorSource(wl)
     table = None
     if not args.rank:
@@ -270,7 +286,7 @@ def run_cpu_baseline(args, wl, kept):
     tokens = sum(len(rec.y) for rec in records) / len(layers)
     scale = wl.n_layers / len(layers)
     return dict(value=tokens / (dt * scale), unit="tok/s", cores=int(blas_threads), kind="oracle",
-                sample=(f"float64 numpy oracle on decode steps 0-{args.cpu_steps - 1} of the same "
+                sample=(f"float64 numpy oracle on decode steps 0-{len(steps) - 1} of the same "
                         f"trace, layers {layers} of {wl.n_layers}, all {wl.n_owners} owners; "
                         f"{dt:.2f} s measured, scaled x{scale:g} to all layers"))
 
@@ -282,12 +298,15 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--layers", type=int, default=None, help="fast-weight layers (default 36)")
     ap.add_argument("--threads", type=int, default=16, help="host threads for input generation")
-    ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
+    ap.add_argument("--cpu-baseline", choices=["on", "off"], default=None,
+                    help="time the oracle on a sample of the workload (default: on for workload 2)")
     ap.add_argument("--cpu-steps", type=int, default=30)
     ap.add_argument("--cpu-layers", type=int, nargs="+", default=[0, 1])
     ap.add_argument("--kernel-events", choices=["on", "off"], default="on")
     ap.add_argument("--streams", type=int, choices=[1, 2], default=1,
                     help="2: READ and WRITE groups on two streams, joined every step")
+    ap.add_argument("--workload", type=int, choices=[1, 2, 3, 4], default=2,
+                    help="2 (default): mixed8-4b-36L; 1 read8-4b; 3 ragged32-4b; 4 prefill8-8b")
     ap.add_argument("--rank", type=int, default=0,
                     help="0: fast-weight state (default); r > 0: the rank-r adapter backend")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
@@ -315,7 +334,9 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": args.calibrate_copy, "launches": 5}))
         return
     from rwttt_inputs import workload
-    wl = workload(2)
+    if args.cpu_baseline is None:
+        args.cpu_baseline = "on" if args.workload == 2 else "off"
+    wl = workload(args.workload)
     layers = list(range(wl.n_layers if args.layers is None else args.layers))
 
     g = run_gpu(args, wl, layers)
@@ -326,19 +347,20 @@ def main():
         "value": round(tok_s, 2),
         "unit": "tok/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(1e3 * g["elapsed"] / args.steps, 4),
+        "steps": g["steps"],
+        "warmup": g["warmup"],
+        "ms_per_step": round(1e3 * g["elapsed"] / g["steps"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": f"{wl.name}: 8 streams, {len(layers)} fast-weight layers, d_model "
-                        f"{wl.d_model}, d_ff {wl.d_ff}, bf16 io, fp32 state"
+            "workload": f"{wl.name}: {wl.n_owners} streams, {len(layers)} fast-weight layers, "
+                        f"d_model {wl.d_model}, d_ff {wl.d_ff}, {wl.io_dtype} io, "
+                        f"{wl.state_dtype} state"
                         + (f" as rank-{args.rank} adapters (A, B)" if args.rank else "")
-                        + ", 64 READ steps then one C=64 WRITE per stream, phases staggered by 8",
+                        + f"; {wl.description}",
             "backend": f"delta_adapter rank {args.rank}" if args.rank else "fast_weight",
             "owners": wl.n_owners, "layers": len(layers), "d_model": wl.d_model, "d_ff": wl.d_ff,
             "io": wl.io_dtype, "state": wl.state_dtype, "accumulate": "f32",
