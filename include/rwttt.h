@@ -3,13 +3,14 @@
  * read-write TTT serving (RW-TTT, Yang et al.), for AMD Instinct MI355X
  * (gfx950).
  *
- * Every request r owns a versioned fast-weight delta dW_r per layer, added to
- * the shared down-projection W0 (Section 3, request tuple and Ownership;
- * Section 4.1, FastWeightState).  The library keeps, per (owner, layer), two
- * caller-allocated device slots: the live slot holds the committed version
- * V(r), the other is the shadow that receives a WRITE's dirty candidate.
- * Commit flips which slot is live; rollback forgets the shadow.  Neither
- * copies state.
+ * Every request r owns a versioned state per layer that modifies the shared
+ * down-projection W0 (Section 3, request tuple and Ownership; Section 4.1):
+ * a fast-weight delta dW_r (FastWeightState) or a low-rank pair A_r, B_r
+ * (DeltaAdapterState, Section 4.4).  The library keeps, per (owner, layer),
+ * two caller-allocated device slots: the live slot holds the committed
+ * version V(r), the other is the shadow that receives a WRITE's dirty
+ * candidate.  Commit flips which slot is live; rollback forgets the shadow.
+ * Neither copies state.
  *
  * Conventions for every entry point:
  *  - Returns an rwttt_status: RWTTT_OK (0) or a negative error code.
@@ -21,7 +22,8 @@
  *    and never synchronises the stream it is given.
  *  - Host arrays are read during the call only; the library keeps no pointer
  *    to them, except the config's pointer tables, which it copies.
- *  - Matrices are row-major.  Shapes: W0 and every slot [d_ff, d_model];
+ *  - Matrices are row-major.  Shapes: W0 [d_ff, d_model]; a fast-weight slot
+ *    [d_ff, d_model], an adapter slot A [d_ff, r] then B [r, d_model];
  *    x [n_owners, d_ff]; y [n_owners, d_model]; Z [C, d_ff]; G [C, d_model].
  *  - A context is not thread-safe; use one per host thread.
  */
@@ -284,8 +286,8 @@ rwttt_status rwttt_slot(const rwttt_ctx* ctx, uint32_t owner, uint32_t layer, in
 rwttt_status rwttt_fork(rwttt_ctx* ctx, uint32_t src, uint32_t dst, void* stream);
 
 /* Checkpoint (Section 4.1 snapshot; Section 4.2 CONTROL): copy the owner's
- * committed state, the live slot of every layer (d_ff x d_model state
- * elements, row-major), into dst[layer] and return its version.  dst is a
+ * committed state, the live slot of every layer (rwttt_slot_bytes bytes
+ * each, in the slot layout), into dst[layer] and return its version.  dst is a
  * host array of n_layers caller-owned buffers, each pinned host memory (from
  * hipHostMalloc) or device memory; the copies are asynchronous on `stream`
  * (hipMemcpyAsync), so the caller synchronises before reading them.  An open

@@ -1,6 +1,8 @@
-// Host side of the RW-TTT fast-weight READ/WRITE library: the owner table
-// (versions, live/shadow slot bits, open candidates), the legal-group planner,
-// and the C entry points declared in include/rwttt.h.
+// Host side of the RW-TTT READ/WRITE library: the owner table (versions,
+// live/shadow slot bits, open candidates, tail lengths), the legal-group
+// planner, and the C entry points declared in include/rwttt.h, dispatching to
+// the fast-weight kernels (rwttt_kernels.hip) or the adapter kernels
+// (rwttt_adapter.hip) by the context's backend.
 
 #include <algorithm>
 #include <cstring>
