@@ -58,6 +58,7 @@ def test_tiny_trace_matches_oracle():
 
 READ_CASES = [
     # d_ff, d_model, io, state, n_owners, group
+    (8, 8, "bf16", "f32", 3, [2, 0]),                  # smallest shape
     (256, 64, "f32", "f32", 2, [1, 0]),
     (1000, 264, "bf16", "f32", 12, [3, 0, 7, 11, 5]),
     (1000, 264, "bf16", "bf16", 12, [2, 9, 4, 0, 1, 6, 8, 10, 11]),
@@ -109,6 +110,8 @@ def test_read_matches_oracle(d_ff, d_model, io, state, n_owners, group):
 
 WRITE_CASES = [
     # d_ff, d_model, io, state, chunk, group
+    (8, 8, "bf16", "f32", 1, [1]),                     # smallest shape
+    (8, 8, "bf16", "bf16", 70, [2, 0]),                # smallest shape, GEMM path
     (256, 64, "f32", "f32", 4, [0, 1]),
     (1000, 264, "bf16", "f32", 1, [2]),
     (1000, 264, "bf16", "f32", 17, [0, 3, 1]),
@@ -413,6 +416,43 @@ def test_fork_checkpoint_resume_match_oracle(state):
         for r in range(n_owners):
             ref = O.round_to(O.read_apply(O.widen(X[r], "bf16"), W0, table.D[(r, l)]), "bf16")
             assert O.max_rel_floor(host_f64(y[r], "bf16"), ref) <= BF16_OUT_TOL, (r, l)
+
+
+@pytest.mark.parametrize("chunk", [16, 80])
+def test_largest_group_read_and_write_with_token(chunk):
+    """RWTTT_MAX_GROUP owners in one READ and one WRITE group (kernel argument
+    arrays full), against the oracle; the group is a permutation."""
+    n, d_ff, d_model = R.RWTTT_MAX_GROUP, 264, 136
+    wl = small_workload(d_ff, d_model, "bf16", "f32", n, eta=0.05)
+    say("max group", chunk)
+    src = TensorSource(wl)
+    sess = Session(wl, src)
+    group = list(np.random.default_rng(5).permutation(n))
+    X = draw((n, d_ff), 1.0, "bf16", wl.seed, (93,))
+    xd = to_device(X, "bf16")
+    y = torch.zeros((n, d_model), dtype=torch.bfloat16, device="cuda")
+    read_group(sess, group, 0, xd, y)
+    torch.cuda.synchronize()
+    W0 = O.widen(src.w0(0), "bf16")
+    for r in range(n):
+        ref = O.round_to(O.read_apply(O.widen(X[r], "bf16"), W0, O.widen(src.dw_init(r, 0), "f32")), "bf16")
+        assert O.max_rel_floor(host_f64(y[r], "bf16"), ref) <= BF16_OUT_TOL, r
+    zs = [to_device(draw((chunk, d_ff), 1.0, "bf16", wl.seed, (94, r), absval=True), "bf16") for r in group]
+    gs = [to_device(draw((chunk, d_model), 1.0, "bf16", wl.seed, (95, r)), "bf16") for r in group]
+    y2 = torch.zeros_like(y)
+    assert write_group(sess, group, 0, chunk, zs, gs, x_dev=xd, y_dev=y2) == R.RWTTT_OK
+    assert R.rwttt_commit(sess.ctx, group) == R.RWTTT_OK
+    torch.cuda.synchronize()
+    if chunk > 64:
+        assert torch.equal(y2, y)              # this token is a READ at version v, bit for bit
+    else:
+        for r in range(n):                     # the fused token sums in another order
+            assert O.max_rel_floor(host_f64(y2[r], "bf16"), host_f64(y[r], "bf16")) <= BF16_OUT_TOL, r
+    for i, r in enumerate(group):
+        cand = O.round_to(O.write_candidate(O.widen(src.dw_init(r, 0), "f32"), host_f64(zs[i], "bf16"),
+                                            host_f64(gs[i], "bf16"), wl.eta), "f32")
+        assert O.rel_frobenius(host_f64(sess.live(r, 0), "f32"), cand) <= STATE_TOL, r
+    assert sess.versions() == [1] * n
 
 
 def test_injected_write_failure_rolls_back_exactly():

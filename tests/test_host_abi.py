@@ -9,6 +9,7 @@ import os
 import random
 import re
 import subprocess
+import sys
 
 import pytest
 
@@ -237,3 +238,10 @@ def test_strerror_covers_every_code():
     for code in range(-9, 2):
         assert R.rwttt_strerror(code) != "unknown status"
     assert R.rwttt_strerror(-42) == "unknown status"
+
+
+def test_bench_refuses_more_than_one_gpu():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
