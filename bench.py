@@ -67,35 +67,56 @@ def measured_traffic(records):
     if summ.get("kernel_source_sha256") != sha:
         return None
     table = summ["read_call_bytes_by_group_size"]
-    tot = 0.0
-    for _, b, _, _, _ in records:
+    tot, calls = 0.0, 0
+    for _, b, _, _, _, n in records:
         e = table.get(str(b))
         if e is None:
             return None
-        tot += e["fetch"] + e["write"]
-    return tot / len(records)
+        tot += n * (e["fetch"] + e["write"])
+        calls += n
+    return tot / calls
 
 
 class LaunchTimer:
-    """HIP events around every launch, on torch's current stream."""
+    """HIP events around runs of launches of one kind.
+
+    ``launch(kind, count, chunk, stream)`` is called before every library
+    call; consecutive calls of the same kind, group size and chunk on one
+    stream form one span between two events recorded on that stream, and
+    ``close()`` ends the open spans.  An event pair per call would put a
+    marker between every two kernels; a span per run of calls keeps the
+    stream as the serving loop issues it.  The average call duration of a
+    span is its elapsed time over its number of calls (inter-call gaps
+    included, so the figure is conservative).
+    """
 
     def __init__(self, torch, streams=()):
         self.torch = torch
-        self.records = []
-        self._open = None
+        self.records = []            # (kind, count, chunk, start event, end event, calls)
+        self._open = {}
         self._streams = {s.cuda_stream: s for s in streams}
 
-    def begin(self, kind, count, chunk, stream):
+    def launch(self, kind, count, chunk, stream):
+        cur = self._open.get(stream)
+        if cur is not None and cur[:3] == [kind, count, chunk]:
+            cur[5] += 1
+            return
+        if cur is not None:
+            self._close(stream)
         st = self._stream(stream)
         e = self.torch.cuda.Event(enable_timing=True)
         e.record(st)
-        self._open = (kind, count, chunk, e, st)
+        self._open[stream] = [kind, count, chunk, e, st, 1]
 
-    def end(self):
-        kind, count, chunk, s, st = self._open
-        e = self.torch.cuda.Event(enable_timing=True)
-        e.record(st)
-        self.records.append((kind, count, chunk, s, e))
+    def close(self):
+        for stream in list(self._open):
+            self._close(stream)
+
+    def _close(self, stream):
+        kind, count, chunk, e0, st, n = self._open.pop(stream)
+        e1 = self.torch.cuda.Event(enable_timing=True)
+        e1.record(st)
+        self.records.append((kind, count, chunk, e0, e1, n))
 
     def _stream(self, handle):
         if handle in self._streams:
@@ -110,28 +131,30 @@ class LaunchTimer:
             recs = [r for r in self.records if r[0] == kind]
             if not recs:
                 continue
-            ms = sum(s.elapsed_time(e) for _, _, _, s, e in recs)
+            ms = sum(s.elapsed_time(e) for _, _, _, s, e, _ in recs)
+            calls = sum(n for *_, n in recs)
             if rank:
                 # adapter: W0 once, each owner's A and B, x and y; WRITE reads the live
                 # factors, writes the shadow and reads Z and G
                 tok = kind != "write"
-                rb = sum(K * N * io + b * (K + N) * (rank * st + io) for _, b, _, _, _ in recs)
-                rf = sum(b * (2.0 * K * N + 2.0 * rank * (K + N)) for _, b, _, _, _ in recs)
-                wb = sum(b * (2 * (K + N) * rank * st + io * c * (K + N)) for _, b, c, _, _ in recs)
-                wf = sum(4.0 * b * c * rank * (K + N) for _, b, c, _, _ in recs)
+                rb = sum(n * (K * N * io + b * (K + N) * (rank * st + io)) for _, b, _, _, _, n in recs)
+                rf = sum(n * b * (2.0 * K * N + 2.0 * rank * (K + N)) for _, b, _, _, _, n in recs)
+                wb = sum(n * b * (2 * (K + N) * rank * st + io * c * (K + N)) for _, b, c, _, _, n in recs)
+                wf = sum(n * 4.0 * b * c * rank * (K + N) for _, b, c, _, _, n in recs)
                 byt = (rb if tok else 0) + (wb if kind != "read" else 0)
                 flop = (rf if tok else 0) + (wf if kind != "read" else 0)
             elif kind == "read":
-                byt = sum(K * N * (io + b * st) + b * io * (K + N) for _, b, _, _, _ in recs)
-                flop = sum(4.0 * b * K * N for _, b, _, _, _ in recs)
+                byt = sum(n * (K * N * (io + b * st) + b * io * (K + N)) for _, b, _, _, _, n in recs)
+                flop = sum(n * 4.0 * b * K * N for _, b, _, _, _, n in recs)
             else:
                 # live read + shadow write + Z, G; with the token also W0 once and x, y
                 tok = kind == "write_token"
-                byt = sum(b * (2 * st * K * N + io * c * (K + N))
-                          + (K * N * io + b * io * (K + N) if tok else 0) for _, b, c, _, _ in recs)
-                flop = sum(2.0 * b * c * K * N + (4.0 * b * K * N if tok else 0)
-                           for _, b, c, _, _ in recs)
-            out[kind] = dict(launches=len(recs), total_ms=ms, avg_us=1e3 * ms / len(recs),
+                byt = sum(n * (b * (2 * st * K * N + io * c * (K + N))
+                               + (K * N * io + b * io * (K + N) if tok else 0))
+                          for _, b, c, _, _, n in recs)
+                flop = sum(n * (2.0 * b * c * K * N + (4.0 * b * K * N if tok else 0))
+                           for _, b, c, _, _, n in recs)
+            out[kind] = dict(launches=calls, total_ms=ms, avg_us=1e3 * ms / calls,
                              bytes=byt, flops=flop, records=recs,
                              gbs=byt / (ms * 1e-3) / 1e9, tflops=flop / (ms * 1e-3) / 1e12)
         return out

@@ -194,8 +194,9 @@ class Session:
         ``StreamPair``: READ groups then go on its read stream and WRITE groups
         (update with its token) on its write stream, so groups of disjoint
         owners overlap on the device; the pair is joined both ways at the end
-        of the step.  ``timer``, if given, has begin(kind, count, chunk,
-        stream) / end() called around every launch.
+        of the step.  ``timer``, if given, has launch(kind, count, chunk,
+        stream) called before every library call and close() after every
+        group.
         """
         pair = stream if isinstance(stream, StreamPair) else None
         s_read = pair.read if pair else stream
@@ -223,12 +224,10 @@ class Session:
                     gs = [zg_ptrs[r][1][i] for r in owners]
                     tok = emit or bool(self.tails)
                     if timer is not None:
-                        timer.begin("write_token" if tok else "write", g.count, chunk, stream)
+                        timer.launch("write_token" if tok else "write", g.count, chunk, stream)
                     st = R.rwttt_write(self.ctx, g, plan.owner_map_c, i, chunk, zs, gs, wl.eta,
                                        x_ptrs[i] if tok else 0, y_ptrs[i] if tok else 0,
                                        stream)
-                    if timer is not None:
-                        timer.end()
                     statuses.append(st)
                     if st == R.RWTTT_OK:
                         need_token = False
@@ -239,15 +238,15 @@ class Session:
                     # the token at the unchanged version v (a READ step also appends
                     # its input to the owner's tail)
                     if timer is not None:
-                        timer.begin("read", g.count, 0, stream)
+                        timer.launch("read", g.count, 0, stream)
                     fn = R.rwttt_read_append if self.tails and not is_write else R.rwttt_read
                     st = fn(self.ctx, g, plan.owner_map_c, i, x_ptrs[i], y_ptrs[i], stream)
-                    if timer is not None:
-                        timer.end()
                     if st != R.RWTTT_OK:
                         raise R.RwtttError(st, "rwttt_read")
             if is_write:
                 write_groups.append((owners, failed))
+            if timer is not None:
+                timer.close()
         if pair is not None:
             pair.join()
         committed, rolled = [], []
