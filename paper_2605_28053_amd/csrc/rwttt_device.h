@@ -57,21 +57,27 @@ template <int N> __device__ __forceinline__ void load_n(const uint16_t* p, float
   }
 }
 
-template <int N> __device__ __forceinline__ void store_n(float* p, const float (&v)[N]) {
-#pragma unroll
-  for (int i = 0; i < N; i += 4)
-    *reinterpret_cast<float4*>(p + i) = make_float4(v[i], v[i + 1], v[i + 2], v[i + 3]);
-}
-template <int N> __device__ __forceinline__ void store_n(uint16_t* p, const float (&v)[N]) {
-  static_assert(N == 4, "bf16 stores are 4 wide");
-  uint2 t;
-  t.x = bf16x2_rne(v[0], v[1]);
-  t.y = bf16x2_rne(v[2], v[3]);
-  *reinterpret_cast<uint2*>(p) = t;
-}
-
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// NT: a streaming (non-temporal) store, for state that is not read again soon.
+template <int N, bool NT = false>
+__device__ __forceinline__ void store_n(float* p, const float (&v)[N]) {
+#pragma unroll
+  for (int i = 0; i < N; i += 4) {
+    const f32x4_t t = {v[i], v[i + 1], v[i + 2], v[i + 3]};
+    if (NT) __builtin_nontemporal_store(t, reinterpret_cast<f32x4_t*>(p + i));
+    else *reinterpret_cast<f32x4_t*>(p + i) = t;
+  }
+}
+template <int N, bool NT = false>
+__device__ __forceinline__ void store_n(uint16_t* p, const float (&v)[N]) {
+  static_assert(N == 4, "bf16 stores are 4 wide");
+  const u32x2_t t = {bf16x2_rne(v[0], v[1]), bf16x2_rne(v[2], v[3])};
+  if (NT) __builtin_nontemporal_store(t, reinterpret_cast<u32x2_t*>(p));
+  else *reinterpret_cast<u32x2_t*>(p) = t;
+}
 
 // N elements of T held packed in 32-bit words, converted to fp32 on use.
 template <typename T, int N> struct Packed {

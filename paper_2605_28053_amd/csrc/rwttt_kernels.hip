@@ -347,7 +347,7 @@ write_stream_kernel(const WriteParams p) {
         float o[4];
 #pragma unroll
         for (int c = 0; c < 4; ++c) o[c] = lv[rr].get(c) + eta * out[row * kSTN + lane * 4 + c];
-        store_n<4>(shadow + size_t(m) * p.d_model + ncol, o);
+        store_n<4, true>(shadow + size_t(m) * p.d_model + ncol, o);
       }
     }
     if (TOKEN) {
@@ -570,7 +570,7 @@ __global__ void __launch_bounds__(kGThreads, 1) write_gemm_kernel(const WritePar
       const float o[SC] = {lv[rr].get(0) + eta * a4.x, lv[rr].get(1) + eta * a4.y,
                            lv[rr].get(2) + eta * a4.z, lv[rr].get(3) + eta * a4.w};
       if (interior || (mrow0 + rr < p.d_ff && ncol_ok))
-        store_n<SC>(shadow + size_t(mrow0 + rr) * p.d_model + ncol, o);
+        store_n<SC, true>(shadow + size_t(mrow0 + rr) * p.d_model + ncol, o);
       // this row's register slot now takes the same row of the next pass
       if (ps + 1 < kGTM / 64) {
         if (interior || (nrow0 + rr < p.d_ff && ncol_ok))
@@ -615,7 +615,7 @@ __global__ void __launch_bounds__(256) write_valu_kernel(const WriteParams p) {
   float out[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) out[i] = lv[i] + p.eta * a[i];
-  store_n<4>(shadow + size_t(m) * p.d_model + n, out);
+  store_n<4, true>(shadow + size_t(m) * p.d_model + n, out);
 }
 
 // ---------------------------------------------------------------------------
