@@ -245,3 +245,16 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_plain_c_client_builds_against_the_header_and_runs(tmp_path):
+    """The header is C (not only C++): a C11 client compiles with gcc, links the
+    library and drives planning and the owner table on a host-only context."""
+    exe = str(tmp_path / "abi_host_check")
+    libdir = os.path.dirname(R.LIB_PATH)
+    subprocess.run(["gcc", "-std=c11", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"),
+                    os.path.join(ROOT, "tests", "c", "abi_host_check.c"), "-L", libdir, "-lrwttt",
+                    f"-Wl,-rpath,{libdir}", "-o", exe], check=True, capture_output=True, text=True)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.strip() == "ok"
