@@ -73,10 +73,17 @@ __device__ __forceinline__ void store_n(float* p, const float (&v)[N]) {
 }
 template <int N, bool NT = false>
 __device__ __forceinline__ void store_n(uint16_t* p, const float (&v)[N]) {
-  static_assert(N == 4, "bf16 stores are 4 wide");
-  const u32x2_t t = {bf16x2_rne(v[0], v[1]), bf16x2_rne(v[2], v[3])};
-  if (NT) __builtin_nontemporal_store(t, reinterpret_cast<u32x2_t*>(p));
-  else *reinterpret_cast<u32x2_t*>(p) = t;
+  static_assert(N == 4 || N == 8, "bf16 stores are 4 or 8 wide");
+  if constexpr (N == 4) {
+    const u32x2_t t = {bf16x2_rne(v[0], v[1]), bf16x2_rne(v[2], v[3])};
+    if (NT) __builtin_nontemporal_store(t, reinterpret_cast<u32x2_t*>(p));
+    else *reinterpret_cast<u32x2_t*>(p) = t;
+  } else {
+    const u32x4_t t = {bf16x2_rne(v[0], v[1]), bf16x2_rne(v[2], v[3]), bf16x2_rne(v[4], v[5]),
+                       bf16x2_rne(v[6], v[7])};
+    if (NT) __builtin_nontemporal_store(t, reinterpret_cast<u32x4_t*>(p));
+    else *reinterpret_cast<u32x4_t*>(p) = t;
+  }
 }
 
 // N elements of T held packed in 32-bit words, converted to fp32 on use.

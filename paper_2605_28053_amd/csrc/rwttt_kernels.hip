@@ -386,109 +386,175 @@ write_stream_kernel(const WriteParams p) {
 // ---------------------------------------------------------------------------
 //
 // At C = 512 the update does 2C flop per state element and is near the MFMA
-// ridge, so it is organised as a GEMM.  Block tile 256 rows (d_ff) x 256
-// columns (d_model), eight waves of 64 x 128 (2 x 4 MFMA 32x32x16 blocks,
-// 128 accumulators per lane).  Ranks are consumed in chunks of 64.  Z and G
-// arrive rank-major, so each thread loads an 8 x 8 block of 16-bit values
-// (8 ranks x 8 columns) with 16-byte loads and transposes it in registers
-// (v_perm_b32) into 8 rank-contiguous rows.  LDS rows are 64 ranks (128 B)
-// with the eight 16-byte groups of row r stored in slot (group ^ (r & 7)):
-// the transposed stores and the MFMA operand reads are then free of bank
-// conflicts.  The next chunk's global loads are in flight while the MFMAs
-// consume the current one.  Each XCD keeps a fixed set of column tiles (so
-// its G tiles stay in its L2) and walks the (owner, row tile) list.  The
-// epilogue moves the accumulators through LDS in 64-row passes so that all
-// eight waves read live and write shadow as contiguous rows, converting to
-// bf16 with the hardware packed convert.
+// ridge, so it is organised as a GEMM: D = Z^T G per 256-row (d_ff) x
+// 128-column (d_model) tile, four waves of 64 x 128 (2 x 4 MFMA 32x32x16
+// blocks, 128 accumulators per lane), two blocks per CU.  The two blocks of
+// a CU run independently, so one block's HBM-bound epilogue (read live,
+// write shadow) overlaps the other's MFMA main loop.
+//
+// Operand staging uses no registers: Z and G arrive rank-major and are
+// copied as they are, 16 bytes per lane, by buffer loads that write LDS
+// directly (lane l of a load lands at LDS offset 16 l).  Ranks are consumed
+// in stages of 32 (A: 32 x 256 of Z, B: 32 x 128 of G, 24 KB), three stages
+// in flight; each wait names how many newer copies may still be outstanding.  The buffer range check turns every
+// 16-byte group outside the chunk or the matrix into zeros, so ragged tiles
+// need no other code.  The MFMA operands (8 consecutive ranks of one row m or
+// column n) are read back with the transposing LDS read ds_read_b64_tr_b16:
+// within each 16-lane group, lane i receives element i % 4 of the 8-byte runs
+// addressed by lanes 4j + i / 4, so lanes 4j + q address rank row j, columns
+// 4q..4q+3 and two such reads give one operand.  The 16-byte groups of rank
+// row r sit in slot (group ^ swz(r & 3)), swz = {0, 10, 4, 14}, chosen so
+// that every transposing read is free of bank conflicts.
+//
+// Epilogue: each wave passes its own accumulators through a private 8 KB LDS
+// region in 16-row steps (no block barrier), then reads back whole rows of
+// 8 columns per lane, adds eta * D to the live rows (prefetched one step
+// ahead) and stores the shadow rows, rounding to bf16 with the hardware
+// packed convert.
 
-constexpr int kGTM = 256;
-constexpr int kGTN = 256;
-constexpr int kGKC = 64;                                  // ranks per chunk = LDS row length
-constexpr int kGThreads = 512;                            // 8 waves: 4 in m x 2 in n, 64 x 128 each
+constexpr int kGTM = 256;                                 // rows (d_ff) per tile
+constexpr int kGTN = 128;                                 // columns (d_model) per tile
+constexpr int kGKC = 32;                                  // ranks per LDS stage
+constexpr int kGThreads = 256;                            // 4 waves of 64 x 128
+constexpr int kGStageA = kGKC * kGTM;                     // bf16 elements of Z per stage
+constexpr int kGStage = kGStageA + kGKC * kGTN;           // 24 KB per stage
+constexpr int kGUnitsA = kGStageA * 2 / 1024;             // 1 KB copies of Z per stage (16)
+constexpr int kGUnits = kGStage * 2 / 1024;               // 1 KB copies per stage (24)
+constexpr int kGCopies = kGUnits / 4;                     // copies per wave per stage (6)
+constexpr int kGColGroups = 8;                            // XCD -> column-tile groups
 
-// Transpose an 8 x 8 block of 16-bit values: row k of the input is r[k] (8
-// values, two per word); output j holds column j as 8 values, two per word.
-__device__ __forceinline__ void transpose8x8(const uint4 (&r)[8], uint4 (&o)[8]) {
-  const uint32_t* w[8];
-#pragma unroll
-  for (int k = 0; k < 8; ++k) w[k] = reinterpret_cast<const uint32_t*>(&r[k]);
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    // even j: low halves of (row 2q, row 2q+1); odd j: high halves
-    const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
-    o[j] = make_uint4(__builtin_amdgcn_perm(w[1][j >> 1], w[0][j >> 1], sel),
-                      __builtin_amdgcn_perm(w[3][j >> 1], w[2][j >> 1], sel),
-                      __builtin_amdgcn_perm(w[5][j >> 1], w[4][j >> 1], sel),
-                      __builtin_amdgcn_perm(w[7][j >> 1], w[6][j >> 1], sel));
-  }
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
+
+__device__ __forceinline__ int gemm_swz(int r) { return ((r & 3) * 2) ^ ((r & 1) << 3); }
+
+// s_waitcnt with vmcnt(N) and lgkmcnt(0), expcnt left open; no memory access
+// moves across it
+template <int N>
+__device__ __forceinline__ void gemm_wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+  asm volatile("" ::: "memory");
 }
 
-// bf16 offset of 16-byte group g of LDS row r (rows of kGKC ranks, swizzled).
-__device__ __forceinline__ int gemm_lds_off(int r, int g) { return r * kGKC + ((g ^ (r & 7)) << 3); }
-
-// Loads one 8 x 8 block (8 ranks from c, 8 columns from col) of a rank-major
-// [chunk, ld] operand; zeros outside unless the block is known to be inside.
-__device__ __forceinline__ void gemm_load_block(const uint16_t* src, size_t ld, int c, int chunk,
-                                                int col, int lim, bool inside, uint4 (&st)[8]) {
-  const uint16_t* q = src + size_t(c) * ld + col;
-  if (inside) {
-#pragma unroll
-    for (int r = 0; r < 8; ++r) st[r] = *reinterpret_cast<const uint4*>(q + size_t(r) * ld);
-  } else {
-#pragma unroll
-    for (int r = 0; r < 8; ++r)
-      st[r] = (c + r < chunk && col < lim) ? *reinterpret_cast<const uint4*>(q + size_t(r) * ld)
-                                           : make_uint4(0, 0, 0, 0);
-  }
+__device__ __forceinline__ void gemm_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
-__device__ __forceinline__ void gemm_store_block(uint16_t* lds, int row0, int g, const uint4 (&st)[8]) {
-  uint4 o[8];
-  transpose8x8(st, o);
-#pragma unroll
-  for (int j = 0; j < 8; ++j) *reinterpret_cast<uint4*>(&lds[gemm_lds_off(row0 + j, g)]) = o[j];
+typedef short i16x8_t __attribute__((ext_vector_type(8)));
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+// Buffer descriptor of `bytes` bytes at p: no stride, 32-bit data format
+// (accesses at or past `bytes` return zeros and touch no memory).
+__device__ __forceinline__ i32x4_t gemm_rsrc(const void* p, int bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(p);
+  return i32x4_t{int(uint32_t(a)), int(uint32_t(a >> 32) & 0xffffu), bytes, 0x00020000};
+}
+
+// One 1 KB stage copy: lane l's 16 bytes at byte offset voff of the buffer go
+// to LDS at dst + 16 l.  Issued as inline assembly so that the compiler does
+// not add its own (conservative) waits for LDS copies: every read of a stage
+// is preceded by an explicit vmcnt wait and a barrier.
+__device__ __forceinline__ void gemm_copy(uint16_t* dst, uint32_t voff, i32x4_t rsrc) {
+  const uint32_t lds = uint32_t(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint16_t*)dst));
+  // the descriptor and the LDS address are wave-uniform: keep them in SGPRs
+  const i32x4_t r = {__builtin_amdgcn_readfirstlane(rsrc[0]), __builtin_amdgcn_readfirstlane(rsrc[1]),
+                     __builtin_amdgcn_readfirstlane(rsrc[2]), __builtin_amdgcn_readfirstlane(rsrc[3])};
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(r) : "memory", "m0");
+#pragma clang diagnostic pop
+}
+
+// One MFMA operand: 8 consecutive ranks (two transposing reads, 4 rank rows
+// apart) of the row or column that this lane owns; ROW = LDS row length.
+template <int ROW>
+__device__ __forceinline__ bf16x8_t gemm_operand(const uint16_t* lds, int off) {
+  const i16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(lds + off));
+  const i16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(lds + off + 4 * ROW));
+  return __builtin_bit_cast(bf16x8_t, i16x8_t(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7)));
 }
 
 template <typename ST>
-__global__ void __launch_bounds__(kGThreads, 1) write_gemm_kernel(const WriteParams p) {
-  constexpr int SC = 4;                                                   // columns per lane
-  __shared__ __attribute__((aligned(16))) uint16_t lds[(kGTM + kGTN) * kGKC];   // 64 KB
-  float* out = reinterpret_cast<float*>(lds);                             // [64][kGTN] in the epilogue
-  uint16_t* A = lds;                                                      // [kGTM][kGKC]
-  uint16_t* B = lds + kGTM * kGKC;                                        // [kGTN][kGKC]
+__global__ void __launch_bounds__(kGThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+write_gemm_kernel(const WriteParams p) {
+  __shared__ __attribute__((aligned(16))) uint16_t s0[kGStage];
+  __shared__ __attribute__((aligned(16))) uint16_t s1[kGStage];
+  __shared__ __attribute__((aligned(16))) uint16_t s2[kGStage];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int half = lane >> 5;
-  // block -> XCD -> (row item, column tile owned by that XCD)
-  const int xcd = blockIdx.x & 7;
-  const int pos = blockIdx.x >> 3;
-  const int ntl8 = (p.ntl + 7) / 8;
-  const int rowid = pos / ntl8;
-  const int nt = (pos - rowid * ntl8) * 8 + xcd;
-  if (nt >= p.ntl || rowid >= p.count * p.mt) return;
-  const int b = rowid / p.mt;
-  const int mt = rowid - b * p.mt;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  // block -> (owner, row tile, column tile).  When the column tiles split
+  // evenly over the 8 XCDs (blocks are dealt to XCDs round-robin), each XCD
+  // keeps its own column tiles, so their G rows stay in that XCD's L2.
+  int b, mt, nt;
+  if ((p.ntl & 7) == 0) {
+    const int xcd = blockIdx.x & 7, pos = blockIdx.x >> 3, ntg = p.ntl >> 3;
+    const int rowid = pos / ntg;
+    nt = xcd * ntg + (pos - rowid * ntg);
+    b = rowid / p.mt;
+    mt = rowid - b * p.mt;
+  } else {
+    const int rowid = blockIdx.x / p.ntl;
+    nt = blockIdx.x - rowid * p.ntl;
+    b = rowid / p.mt;
+    mt = rowid - b * p.mt;
+  }
+  if (b >= p.count) return;
   const int m0 = mt * kGTM;
   const int n0 = nt * kGTN;
-  const bool interior = m0 + kGTM <= p.d_ff && n0 + kGTN <= p.d_model;
   const uint16_t* Z = static_cast<const uint16_t*>(p.z[b]);
   const uint16_t* G = static_cast<const uint16_t*>(p.g[b]);
-  const int wm = wave & 3;
-  const int wn = wave >> 2;
 
-  // staging: threads 0..255 one 8x8 block of G, 256..511 one of Z; consecutive
-  // lanes take different rank groups, so the swizzled stores do not conflict
-  const int sg = tid & 7;
-  const bool is_b = tid < 256;
-  const int srow = ((tid & 255) >> 3) * 8;
-  const uint16_t* ssrc = is_b ? G : Z;
-  const size_t sld = size_t(is_b ? p.d_model : p.d_ff);
-  const int scol = (is_b ? n0 : m0) + srow;
-  const int slim = is_b ? p.d_model : p.d_ff;
-  uint16_t* sdst = is_b ? B : A;
-  uint4 st[8];
+  // Stage copies: wave w moves the 1 KB units w, w + 4, w + 8, w + 12 of Z
+  // (rank rows 2u, 2u + 1) and w, w + 4 of G (rank rows 4u .. 4u + 3).  Lane
+  // l's 16 bytes land at unit offset 16 l, i.e. rank row r, slot s, which
+  // holds column group s ^ swz(r).  Byte offsets are relative to the stage's
+  // first rank row; a group outside the matrix gets an offset past any range.
+  uint32_t voff[kGCopies];
+#pragma unroll
+  for (int t = 0; t < kGCopies; ++t) {
+    const bool za = t < 4;
+    const int u = wave + 4 * (za ? t : t - 4);
+    const int r = za ? 2 * u + (lane >> 5) : 4 * u + (lane >> 4);
+    const int s = za ? (lane & 31) : (lane & 15);
+    const int col = (za ? m0 : n0) + 8 * (s ^ gemm_swz(r));
+    const int lim = za ? p.d_ff : p.d_model;
+    voff[t] = col < lim ? uint32_t(r * lim + col) * 2u : 0x80000000u;
+  }
+  auto issue = [&](uint16_t* st, int c0) {
+    // rank rows past the chunk fall outside the stage's range: zeros
+    const int rows = min(kGKC, p.chunk - c0);
+    const i32x4_t zr = gemm_rsrc(Z + size_t(c0) * p.d_ff, rows * p.d_ff * 2);
+    const i32x4_t gr = gemm_rsrc(G + size_t(c0) * p.d_model, rows * p.d_model * 2);
+#pragma unroll
+    for (int t = 0; t < kGCopies; ++t) {
+      const bool za = t < 4;
+      const int u = wave + 4 * (za ? t : t - 4);
+      gemm_copy(st + (za ? 0 : kGStageA) + u * 512, voff[t], za ? zr : gr);
+    }
+  };
+
+  // operand read offsets (elements, stage-relative) of this lane's fragments
+  const int g4 = lane >> 4;
+  const int eps = g4 & 1;
+  const int hh = g4 >> 1;
+  const int jrow = (lane & 15) >> 2;
+  const int q = lane & 3;
+  const int sw = gemm_swz(jrow);
+  int offa[2], offb[4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+    offa[i] = (8 * hh + jrow) * kGTM + 4 * (q & 1) + (((wave * 8 + i * 4 + 2 * eps + (q >> 1)) ^ sw) << 3);
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    offb[j] = kGStageA + (8 * hh + jrow) * kGTN + 4 * (q & 1) + (((j * 4 + 2 * eps + (q >> 1)) ^ sw) << 3);
 
   f32x16_t acc[2][4];
 #pragma unroll
@@ -496,90 +562,217 @@ __global__ void __launch_bounds__(kGThreads, 1) write_gemm_kernel(const WritePar
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
 
-  // live rows of an epilogue pass (8 per wave), prefetched one step ahead
   const ST* live = static_cast<const ST*>(p.live[b]);
   ST* shadow = static_cast<ST*>(p.shadow[b]);
-  const int ncol = n0 + lane * SC;
+  const float eta = p.eta;
+
+  // fp32 state only: the register epilogue's first live rows are requested
+  // with the first stages and held through the main loop (a lane owns 8
+  // columns of rows (lane >> 4) + 4 rr of each 16-row step)
+  const int c8 = (lane & 15) * 8;
+  const int ncol = n0 + c8;
   const bool ncol_ok = ncol < p.d_model;
-  Packed<ST, SC> lv[8];
-  auto load_live = [&](int ps) {
-    const int mrow0 = m0 + ps * 64 + wave * 8;
+  Packed<ST, 8> lv[4];
+  auto row_of = [&](int sp, int rr) { return m0 + wave * 64 + (sp >> 1) * 32 + (sp & 1) * 16 + (lane >> 4) + 4 * rr; };
+  auto load_live = [&](int sp) {
 #pragma unroll
-    for (int rr = 0; rr < 8; ++rr) {
-      if (interior || (mrow0 + rr < p.d_ff && ncol_ok))
-        load_packed<true>(live + size_t(mrow0 + rr) * p.d_model + ncol, lv[rr]);
+    for (int rr = 0; rr < 4; ++rr) {
+      const int row = row_of(sp, rr);
+      if (row < p.d_ff && ncol_ok)
+        load_packed<true>(live + size_t(row) * p.d_model + ncol, lv[rr]);
       else
         lv[rr].zero();
     }
   };
 
-  const int nchunks = (p.chunk + kGKC - 1) / kGKC;
-  gemm_load_block(ssrc, sld, sg * 8, p.chunk, scol, slim, interior && kGKC <= p.chunk, st);
-  for (int k = 0; k < nchunks; ++k) {
-    gemm_store_block(sdst, srow, sg, st);
-    __syncthreads();
-    if (k + 1 < nchunks)
-      gemm_load_block(ssrc, sld, (k + 1) * kGKC + sg * 8, p.chunk, scol, slim,
-                      interior && (k + 2) * kGKC <= p.chunk, st);
+  // bf16 state: wave w's 64 live rows are copied into freed stages as two
+  // halves of 32 rows x 128 columns (8 KB each), half 0 during the last
+  // stage's MFMAs (into the two stages already consumed), half 1 after it
+  uint16_t* reg[2] = {s0, s0};
+  auto live_copy = [&](uint16_t* dst, int hf) {
+    const int row0 = m0 + wave * 64 + hf * 32;
+    const int rows = max(0, min(32, p.d_ff - row0));
+    const i32x4_t lr = gemm_rsrc(live + size_t(min(row0, p.d_ff)) * p.d_model, rows * p.d_model * 2);
 #pragma unroll
-    for (int ks = 0; ks < kGKC / 16; ++ks) {
-      const int g = ks * 2 + half;
-      bf16x8_t af[2], bfr[4];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_t*>(&A[gemm_lds_off(wm * 64 + i * 32 + (lane & 31), g)]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8_t*>(&B[gemm_lds_off(wn * 128 + j * 32 + (lane & 31), g)]);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    for (int t = 0; t < 8; ++t) {
+      const int r = 4 * t + (lane >> 4);
+      const int col = n0 + 8 * ((lane & 15) ^ gemm_swz(r));
+      const uint32_t off = col < p.d_model ? uint32_t(r * p.d_model + col) * 2u : 0x80000000u;
+      gemm_copy(dst + t * 512, off, lr);
     }
-    __syncthreads();
-  }
+  };
 
-  // Epilogue: pass ps moves tile rows [64 ps, 64 ps + 64) -- the accumulators of the two waves
-  // with wm == ps -- through LDS; then every wave updates 8 whole rows.  Accumulator register
-  // 4q+e of lane l holds D[8q + 4(l/32) + e][l % 32] of its 32x32 block.  Row r of the LDS
-  // tile keeps its columns XOR 32 * ((r >> 2) & 1), so the two half-waves of one write (rows
-  // 4 apart) use different banks; a lane's four columns stay contiguous.
-  const float eta = p.eta;
-  load_live(0);
-#pragma unroll
-  for (int ps = 0; ps < kGTM / 64; ++ps) {
-    if (wm == ps) {
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int row = i * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-            out[row * kGTN + ((wn * 128 + j * 32 + (lane & 31)) ^ (half << 5))] = acc[i][j][r];
-          }
-    }
-    __syncthreads();
-    const int mrow0 = m0 + ps * 64 + wave * 8;
-    const int nrow0 = mrow0 + 64;
-#pragma unroll
-    for (int rr = 0; rr < 8; ++rr) {
-      const int lr = wave * 8 + rr;
-      const float4 a4 = *reinterpret_cast<const float4*>(&out[lr * kGTN + ((lane * SC) ^ (((lr >> 2) & 1) << 5))]);
-      const float o[SC] = {lv[rr].get(0) + eta * a4.x, lv[rr].get(1) + eta * a4.y,
-                           lv[rr].get(2) + eta * a4.z, lv[rr].get(3) + eta * a4.w};
-      if (interior || (mrow0 + rr < p.d_ff && ncol_ok))
-        store_n<SC, true>(shadow + size_t(mrow0 + rr) * p.d_model + ncol, o);
-      // this row's register slot now takes the same row of the next pass
-      if (ps + 1 < kGTM / 64) {
-        if (interior || (nrow0 + rr < p.d_ff && ncol_ok))
-          load_packed<true>(live + size_t(nrow0 + rr) * p.d_model + ncol, lv[rr]);
-        else
-          lv[rr].zero();
+  const int nchunks = (p.chunk + kGKC - 1) / kGKC;
+  auto step = [&](uint16_t* cur, uint16_t* nxt, uint16_t* oth, int k) {
+    // this wave's copies of chunk k are done once at most those of chunk
+    // k + 1 are outstanding; the barrier then covers every wave's copies and
+    // frees the stage read in step k - 1 for chunk k + 2
+    if (k + 1 < nchunks) gemm_wait_vm<kGCopies>();
+    else gemm_wait_vm<0>();
+    gemm_barrier();
+    if (k + 2 < nchunks) issue(nxt, (k + 2) * kGKC);
+    if constexpr (sizeof(ST) == 2) {
+      if (k + 1 == nchunks) {
+        // nxt and oth were read in the two previous steps: 6 free 8 KB slots
+        reg[0] = (wave < 2 ? nxt : oth) + (wave & 1) * 4096;
+        reg[1] = wave < 3 ? cur + wave * 4096 : nxt + 2 * 4096;
+        live_copy(reg[0], 0);
       }
     }
-    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < kGKC / 16; ++ks) {
+      bf16x8_t af[2], bf[4];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) af[i] = gemm_operand<kGTM>(cur, offa[i] + ks * 16 * kGTM);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bf[j] = gemm_operand<kGTN>(cur, offb[j] + ks * 16 * kGTN);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+    }
+  };
+
+  issue(s0, 0);
+  if (nchunks > 1) issue(s1, kGKC);
+  if constexpr (sizeof(ST) == 4) load_live(0);
+  for (int k = 0; k < nchunks; k += 3) {
+    step(s0, s2, s1, k);
+    if (k + 1 < nchunks) step(s1, s0, s2, k + 1);
+    if (k + 2 < nchunks) step(s2, s1, s0, k + 2);
+  }
+  // every wave is done with the stages after this barrier
+  __builtin_amdgcn_s_waitcnt(0xC07F);                      // lgkmcnt(0)
+  gemm_barrier();
+
+  if constexpr (sizeof(ST) == 2) {
+    // bf16 state.  The live halves sit in the freed stages with the same
+    // 16-byte-group swizzle as the operands.  The transposing read then hands each lane live[8a + 4(l/32) + e][l % 32]
+    // for e = 0..3: exactly the rows and column of accumulator registers
+    // 4a+e, so live + eta * D is formed in place.  A 4 x 4 exchange inside
+    // each quad of lanes (two DPP moves) turns 4 rows of one column into 4
+    // columns of one row, stored as 8 bytes.  Loads and stores go through
+    // buffer descriptors clipped to the matrix, so ragged tiles need no
+    // branches and every wave issues a fixed number of memory instructions.
+    live_copy(reg[1], 1);
+    const int jq = (lane >> 2) & 3;                        // read: row in 4; exchange: quad index
+    const int aq = lane & 3;                               // read: 4-column run; quad position
+    int offl[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      offl[j] = (4 * hh + jq) * kGTN + 4 * (aq & 1) + (((4 * j + 2 * eps + (aq >> 1)) ^ gemm_swz(jq)) << 3);
+    // after the exchange this lane holds row 8a + 4 hh + aq, columns
+    // j * 32 + 16 eps + 4 jq .. + 3 of each (j, a) block, written back in
+    // place (8 bytes); LDS requests of one wave complete in order, so every
+    // transposing read of a block precedes the writes into it
+    int offw[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      offw[j] = (4 * hh + aq) * kGTN + 4 * (jq & 1) + (((4 * j + 2 * eps + (jq >> 1)) ^ gemm_swz(aq)) << 3);
+    const bool b1 = lane & 1, b2 = lane & 2;
+    const uint32_t sel_own = b1 ? 0x07060302u : 0x05040100u;
+    const uint32_t sel_snd = b1 ? 0x05040100u : 0x07060302u;
+    // store side: lane l moves 16 bytes (8 columns) of row 4t + l / 16, so
+    // consecutive lanes write consecutive addresses
+    const int srow = lane >> 4;
+    const int scol = n0 + 8 * (lane & 15);
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      // half hf's copies are done once only what was issued after them is
+      // outstanding: the other half's 8 copies, or half 0's 8 stores
+      gemm_wait_vm<8>();
+      i16x4_t lt[4][4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+          lt[j][a] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(reg[hf] + offl[j] + 8 * a * kGTN));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          const i16x4_t l4 = lt[j][a];
+          float f[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            f[e] = __uint_as_float(uint32_t(uint16_t(l4[e])) << 16) + eta * acc[hf][j][4 * a + e];
+          const uint32_t w0 = bf16x2_rne(f[0], f[1]);
+          const uint32_t w1 = bf16x2_rne(f[2], f[3]);
+          // partner lane ^ 2 takes rows {0,1} or {2,3} of this column
+          const uint32_t xa = uint32_t(__builtin_amdgcn_mov_dpp(int(b2 ? w0 : w1), 0x4E, 0xF, 0xF, false));
+          const uint32_t xc = b2 ? w1 : w0;
+          // partner lane ^ 1: keep row (lane & 3), send the other
+          const uint32_t own = __builtin_amdgcn_perm(xa, xc, sel_own);
+          const uint32_t rcv = uint32_t(__builtin_amdgcn_mov_dpp(int(__builtin_amdgcn_perm(xa, xc, sel_snd)), 0xB1,
+                                                                  0xF, 0xF, false));
+          const uint32_t ev = b1 ? rcv : own;
+          const uint32_t od = b1 ? own : rcv;
+          const uint32_t lo = __builtin_amdgcn_perm(od, ev, 0x05040100u);
+          const uint32_t hi = __builtin_amdgcn_perm(od, ev, 0x07060302u);
+          *reinterpret_cast<u32x2_t*>(reg[hf] + offw[j] + 8 * a * kGTN) = u32x2_t{b2 ? hi : lo, b2 ? lo : hi};
+        }
+      }
+      asm volatile("" ::: "memory");
+      const int row0 = m0 + wave * 64 + hf * 32;
+      const int rows = max(0, min(32, p.d_ff - row0));
+      const __amdgpu_buffer_rsrc_t sr = __builtin_amdgcn_make_buffer_rsrc(
+          shadow + size_t(min(row0, p.d_ff)) * p.d_model, (short)0, rows * p.d_model * 2, 0x00020000);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const int r = 4 * t + srow;
+        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(reg[hf] + r * kGTN + (((lane & 15) ^ gemm_swz(r)) << 3));
+        const uint32_t off = scol < p.d_model ? uint32_t(r * p.d_model + scol) * 2u : 0x80000000u;
+        __builtin_amdgcn_raw_buffer_store_b128(v, sr, off, 0, 2);        // non-temporal
+      }
+    }
+  } else {
+    // fp32 state: each wave passes its own accumulators through a private
+    // 8 KB LDS region (16 rows x 128 fp32) in 16-row steps, then every lane
+    // updates 8 contiguous columns of 4 rows.  Accumulator register 4a+e of
+    // lane l holds D[8a + 4(l/32) + e][l % 32] of its 32x32 block; row r of a
+    // region keeps its columns XOR 32 * ((r >> 2) & 1), so the two half-waves
+    // of one write (rows 4 apart) use different banks.  LDS requests of one
+    // wave complete in order, so the region needs no barrier.
+    float* ep = reinterpret_cast<float*>(wave == 1 ? s1 : wave == 2 ? s2 : s0) + (wave == 3 ? 2048 : 0);
+    const int half = lane >> 5;
+#pragma unroll
+    for (int sp = 0; sp < 4; ++sp) {
+      const int i = sp >> 1;
+      const int qh = sp & 1;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int qq = 0; qq < 2; ++qq)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int rl = 8 * qq + 4 * half + e;
+            ep[rl * kGTN + ((j * 32 + (lane & 31)) ^ (half << 5))] = acc[i][j][4 * (2 * qh + qq) + e];
+          }
+      asm volatile("" ::: "memory");
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        const int rl = (lane >> 4) + 4 * rr;
+        const float* src = ep + rl * kGTN + (c8 ^ ((rr & 1) << 5));
+        const f32x4_t a0 = *reinterpret_cast<const f32x4_t*>(src);
+        const f32x4_t a1 = *reinterpret_cast<const f32x4_t*>(src + 4);
+        const float o[8] = {lv[rr].get(0) + eta * a0[0], lv[rr].get(1) + eta * a0[1],
+                            lv[rr].get(2) + eta * a0[2], lv[rr].get(3) + eta * a0[3],
+                            lv[rr].get(4) + eta * a1[0], lv[rr].get(5) + eta * a1[1],
+                            lv[rr].get(6) + eta * a1[2], lv[rr].get(7) + eta * a1[3]};
+        const int row = row_of(sp, rr);
+        if (row < p.d_ff && ncol_ok) store_n<8, true>(shadow + size_t(row) * p.d_model + ncol, o);
+        // this register slot now takes the same row of the next step
+        if (sp + 1 < 4) {
+          const int nrow = row_of(sp + 1, rr);
+          if (nrow < p.d_ff && ncol_ok)
+            load_packed<true>(live + size_t(nrow) * p.d_model + ncol, lv[rr]);
+          else
+            lv[rr].zero();
+        }
+      }
+      asm volatile("" ::: "memory");
+    }
   }
 }
 
@@ -774,9 +967,8 @@ hipError_t launch_write_t(const WriteLaunch& L, hipStream_t stream) {
   if (L.io_bf16) {
     p.mt = (L.d_ff + kGTM - 1) / kGTM;
     p.ntl = (L.d_model + kGTN - 1) / kGTN;
-    const unsigned ntl8 = unsigned((p.ntl + 7) / 8);
-    hipLaunchKernelGGL((write_gemm_kernel<ST>), dim3(unsigned(L.count * p.mt) * ntl8 * 8u),
-                       dim3(kGThreads), 0, stream, p);
+    hipLaunchKernelGGL((write_gemm_kernel<ST>), dim3(unsigned(L.count * p.mt * p.ntl)), dim3(kGThreads), 0,
+                       stream, p);
   } else {
     const size_t per_owner = size_t(L.d_ff) * (L.d_model / 4);
     const unsigned bx = unsigned((per_owner + 255) / 256);
