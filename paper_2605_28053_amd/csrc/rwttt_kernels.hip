@@ -421,7 +421,8 @@ constexpr int kGStage = kGStageA + kGKC * kGTN;           // 24 KB per stage
 constexpr int kGUnitsA = kGStageA * 2 / 1024;             // 1 KB copies of Z per stage (16)
 constexpr int kGUnits = kGStage * 2 / 1024;               // 1 KB copies per stage (24)
 constexpr int kGCopies = kGUnits / 4;                     // copies per wave per stage (6)
-constexpr int kGColGroups = 8;                            // XCD -> column-tile groups
+constexpr int kGColGroups = 4;                            // column-tile groups over the XCDs
+constexpr int kGRowClasses = 8 / kGColGroups;             // row-tile classes over the XCDs
 
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
@@ -490,23 +491,19 @@ write_gemm_kernel(const WriteParams p) {
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // block -> (owner, row tile, column tile).  When the column tiles split
-  // evenly over the 8 XCDs (blocks are dealt to XCDs round-robin), each XCD
-  // keeps its own column tiles, so their G rows stay in that XCD's L2.
-  int b, mt, nt;
-  if ((p.ntl & 7) == 0) {
-    const int xcd = blockIdx.x & 7, pos = blockIdx.x >> 3, ntg = p.ntl >> 3;
-    const int rowid = pos / ntg;
-    nt = xcd * ntg + (pos - rowid * ntg);
-    b = rowid / p.mt;
-    mt = rowid - b * p.mt;
-  } else {
-    const int rowid = blockIdx.x / p.ntl;
-    nt = blockIdx.x - rowid * p.ntl;
-    b = rowid / p.mt;
-    mt = rowid - b * p.mt;
-  }
-  if (b >= p.count) return;
+  // block -> (owner, row tile, column tile).  Blocks are dealt to the 8
+  // XCDs round-robin; XCD x takes column-tile group x % 4 and the row tiles
+  // of parity x / 4, so each G column tile is read by two XCDs and each Z row
+  // tile by four, and consecutive blocks of an XCD share their Z row tile.
+  const int xcd = blockIdx.x & 7;
+  const int pos = blockIdx.x >> 3;
+  const int ntg = (p.ntl + kGColGroups - 1) / kGColGroups;
+  const int mtq = (p.mt + kGRowClasses - 1) / kGRowClasses;
+  const int nt = (xcd % kGColGroups) * ntg + pos % ntg;
+  const int rest = pos / ntg;
+  const int b = rest / mtq;
+  const int mt = (rest - b * mtq) * kGRowClasses + xcd / kGColGroups;
+  if (nt >= p.ntl || mt >= p.mt || b >= p.count) return;
   const int m0 = mt * kGTM;
   const int n0 = nt * kGTN;
   const uint16_t* Z = static_cast<const uint16_t*>(p.z[b]);
@@ -596,7 +593,7 @@ write_gemm_kernel(const WriteParams p) {
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
       const int r = 4 * t + (lane >> 4);
-      const int col = n0 + 8 * ((lane & 15) ^ gemm_swz(r));
+      const int col = n0 + 8 * ((lane & 15) ^ (r & 15));
       const uint32_t off = col < p.d_model ? uint32_t(r * p.d_model + col) * 2u : 0x80000000u;
       gemm_copy(dst + t * 512, off, lr);
     }
@@ -630,7 +627,7 @@ write_gemm_kernel(const WriteParams p) {
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bf[j], af[i], acc[i][j], 0, 0, 0);
     }
   };
 
@@ -647,32 +644,19 @@ write_gemm_kernel(const WriteParams p) {
   gemm_barrier();
 
   if constexpr (sizeof(ST) == 2) {
-    // bf16 state.  The live halves sit in the freed stages with the same
-    // 16-byte-group swizzle as the operands.  The transposing read then hands each lane live[8a + 4(l/32) + e][l % 32]
-    // for e = 0..3: exactly the rows and column of accumulator registers
-    // 4a+e, so live + eta * D is formed in place.  A 4 x 4 exchange inside
-    // each quad of lanes (two DPP moves) turns 4 rows of one column into 4
-    // columns of one row, stored as 8 bytes.  Loads and stores go through
-    // buffer descriptors clipped to the matrix, so ragged tiles need no
-    // branches and every wave issues a fixed number of memory instructions.
+    // bf16 state.  The MFMA is issued as D^T = G^T Z, so accumulator register
+    // 4a+e of block (i, j) holds D[i*32 + l%32][j*32 + 8a + 4(l/32) + e]:
+    // four consecutive columns of one row, the layout of the state itself.
+    // Each lane reads those 8 bytes of live from the copied half (row r's
+    // 16-byte groups sit in slot (group ^ (r & 15)), so the 16 rows of a
+    // half-wave hit distinct banks), forms live + eta * D and writes the
+    // bf16 result back in place; whole rows are then read back and stored.
+    // Loads and stores go through buffer descriptors clipped to the matrix,
+    // so ragged tiles need no branches and every wave issues a fixed number
+    // of memory instructions.
     live_copy(reg[1], 1);
-    const int jq = (lane >> 2) & 3;                        // read: row in 4; exchange: quad index
-    const int aq = lane & 3;                               // read: 4-column run; quad position
-    int offl[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      offl[j] = (4 * hh + jq) * kGTN + 4 * (aq & 1) + (((4 * j + 2 * eps + (aq >> 1)) ^ gemm_swz(jq)) << 3);
-    // after the exchange this lane holds row 8a + 4 hh + aq, columns
-    // j * 32 + 16 eps + 4 jq .. + 3 of each (j, a) block, written back in
-    // place (8 bytes); LDS requests of one wave complete in order, so every
-    // transposing read of a block precedes the writes into it
-    int offw[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      offw[j] = (4 * hh + aq) * kGTN + 4 * (jq & 1) + (((4 * j + 2 * eps + (jq >> 1)) ^ gemm_swz(aq)) << 3);
-    const bool b1 = lane & 1, b2 = lane & 2;
-    const uint32_t sel_own = b1 ? 0x07060302u : 0x05040100u;
-    const uint32_t sel_snd = b1 ? 0x05040100u : 0x07060302u;
+    const int ml = lane & 31;                              // row of the half this lane updates
+    const int h4 = (lane >> 5) * 4;                        // column offset within the 8-column group
     // store side: lane l moves 16 bytes (8 columns) of row 4t + l / 16, so
     // consecutive lanes write consecutive addresses
     const int srow = lane >> 4;
@@ -682,37 +666,25 @@ write_gemm_kernel(const WriteParams p) {
       // half hf's copies are done once only what was issued after them is
       // outstanding: the other half's 8 copies, or half 0's 8 stores
       gemm_wait_vm<8>();
-      i16x4_t lt[4][4];
+      typedef __attribute__((address_space(3))) u32x2_t lds_u32x2_t;
+      u32x2_t lt[4][4];
 #pragma unroll
       for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int a = 0; a < 4; ++a)
-          lt[j][a] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(reg[hf] + offl[j] + 8 * a * kGTN));
+          lt[j][a] = *(const lds_u32x2_t*)(reg[hf] + ml * kGTN + (((4 * j + a) ^ (ml & 15)) << 3) + h4);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int a = 0; a < 4; ++a) {
-          const i16x4_t l4 = lt[j][a];
-          float f[4];
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            f[e] = __uint_as_float(uint32_t(uint16_t(l4[e])) << 16) + eta * acc[hf][j][4 * a + e];
-          const uint32_t w0 = bf16x2_rne(f[0], f[1]);
-          const uint32_t w1 = bf16x2_rne(f[2], f[3]);
-          // partner lane ^ 2 takes rows {0,1} or {2,3} of this column
-          const uint32_t xa = uint32_t(__builtin_amdgcn_mov_dpp(int(b2 ? w0 : w1), 0x4E, 0xF, 0xF, false));
-          const uint32_t xc = b2 ? w1 : w0;
-          // partner lane ^ 1: keep row (lane & 3), send the other
-          const uint32_t own = __builtin_amdgcn_perm(xa, xc, sel_own);
-          const uint32_t rcv = uint32_t(__builtin_amdgcn_mov_dpp(int(__builtin_amdgcn_perm(xa, xc, sel_snd)), 0xB1,
-                                                                  0xF, 0xF, false));
-          const uint32_t ev = b1 ? rcv : own;
-          const uint32_t od = b1 ? own : rcv;
-          const uint32_t lo = __builtin_amdgcn_perm(od, ev, 0x05040100u);
-          const uint32_t hi = __builtin_amdgcn_perm(od, ev, 0x07060302u);
-          *reinterpret_cast<u32x2_t*>(reg[hf] + offw[j] + 8 * a * kGTN) = u32x2_t{b2 ? hi : lo, b2 ? lo : hi};
+          const f32x16_t& d = acc[hf][j];
+          const float f0 = __uint_as_float(lt[j][a][0] << 16) + eta * d[4 * a + 0];
+          const float f1 = __uint_as_float(lt[j][a][0] & 0xffff0000u) + eta * d[4 * a + 1];
+          const float f2 = __uint_as_float(lt[j][a][1] << 16) + eta * d[4 * a + 2];
+          const float f3 = __uint_as_float(lt[j][a][1] & 0xffff0000u) + eta * d[4 * a + 3];
+          *(lds_u32x2_t*)(reg[hf] + ml * kGTN + (((4 * j + a) ^ (ml & 15)) << 3) + h4) =
+              u32x2_t{bf16x2_rne(f0, f1), bf16x2_rne(f2, f3)};
         }
-      }
       asm volatile("" ::: "memory");
       const int row0 = m0 + wave * 64 + hf * 32;
       const int rows = max(0, min(32, p.d_ff - row0));
@@ -721,7 +693,7 @@ write_gemm_kernel(const WriteParams p) {
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
         const int r = 4 * t + srow;
-        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(reg[hf] + r * kGTN + (((lane & 15) ^ gemm_swz(r)) << 3));
+        const u32x4_t v = *reinterpret_cast<const u32x4_t*>(reg[hf] + r * kGTN + (((lane & 15) ^ (r & 15)) << 3));
         const uint32_t off = scol < p.d_model ? uint32_t(r * p.d_model + scol) * 2u : 0x80000000u;
         __builtin_amdgcn_raw_buffer_store_b128(v, sr, off, 0, 2);        // non-temporal
       }
@@ -730,32 +702,35 @@ write_gemm_kernel(const WriteParams p) {
     // fp32 state: each wave passes its own accumulators through a private
     // 8 KB LDS region (16 rows x 128 fp32) in 16-row steps, then every lane
     // updates 8 contiguous columns of 4 rows.  Accumulator register 4a+e of
-    // lane l holds D[8a + 4(l/32) + e][l % 32] of its 32x32 block; row r of a
-    // region keeps its columns XOR 32 * ((r >> 2) & 1), so the two half-waves
-    // of one write (rows 4 apart) use different banks.  LDS requests of one
-    // wave complete in order, so the region needs no barrier.
+    // block (i, j) holds D[i*32 + l%32][j*32 + 8a + 4(l/32) + e]: the lanes
+    // whose row falls in the step write those 16 bytes.  Row r of a region
+    // keeps its 16-byte units XOR (r & 15), so the rows of one write hit
+    // distinct banks.  LDS requests of one wave complete in order, so the
+    // region needs no barrier.
     float* ep = reinterpret_cast<float*>(wave == 1 ? s1 : wave == 2 ? s2 : s0) + (wave == 3 ? 2048 : 0);
-    const int half = lane >> 5;
+    const int hu = lane >> 5;                              // 16-byte unit within the 8-column group
 #pragma unroll
     for (int sp = 0; sp < 4; ++sp) {
       const int i = sp >> 1;
       const int qh = sp & 1;
+      if (((lane & 31) >> 4) == qh) {
+        const int rl = (lane & 15);
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < 4; ++j)
 #pragma unroll
-        for (int qq = 0; qq < 2; ++qq)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int rl = 8 * qq + 4 * half + e;
-            ep[rl * kGTN + ((j * 32 + (lane & 31)) ^ (half << 5))] = acc[i][j][4 * (2 * qh + qq) + e];
+          for (int a = 0; a < 4; ++a) {
+            const int u = 8 * j + 2 * a + hu;
+            *reinterpret_cast<f32x4_t*>(ep + rl * kGTN + ((u ^ rl) << 2)) =
+                f32x4_t{acc[i][j][4 * a], acc[i][j][4 * a + 1], acc[i][j][4 * a + 2], acc[i][j][4 * a + 3]};
           }
+      }
       asm volatile("" ::: "memory");
 #pragma unroll
       for (int rr = 0; rr < 4; ++rr) {
         const int rl = (lane >> 4) + 4 * rr;
-        const float* src = ep + rl * kGTN + (c8 ^ ((rr & 1) << 5));
-        const f32x4_t a0 = *reinterpret_cast<const f32x4_t*>(src);
-        const f32x4_t a1 = *reinterpret_cast<const f32x4_t*>(src + 4);
+        const int u0 = 2 * (lane & 15);
+        const f32x4_t a0 = *reinterpret_cast<const f32x4_t*>(ep + rl * kGTN + ((u0 ^ (rl & 15)) << 2));
+        const f32x4_t a1 = *reinterpret_cast<const f32x4_t*>(ep + rl * kGTN + (((u0 + 1) ^ (rl & 15)) << 2));
         const float o[8] = {lv[rr].get(0) + eta * a0[0], lv[rr].get(1) + eta * a0[1],
                             lv[rr].get(2) + eta * a0[2], lv[rr].get(3) + eta * a0[3],
                             lv[rr].get(4) + eta * a1[0], lv[rr].get(5) + eta * a1[1],
@@ -967,7 +942,9 @@ hipError_t launch_write_t(const WriteLaunch& L, hipStream_t stream) {
   if (L.io_bf16) {
     p.mt = (L.d_ff + kGTM - 1) / kGTM;
     p.ntl = (L.d_model + kGTN - 1) / kGTN;
-    hipLaunchKernelGGL((write_gemm_kernel<ST>), dim3(unsigned(L.count * p.mt * p.ntl)), dim3(kGThreads), 0,
+    const unsigned ntg = unsigned((p.ntl + kGColGroups - 1) / kGColGroups);
+    const unsigned mtq = unsigned((p.mt + kGRowClasses - 1) / kGRowClasses);
+    hipLaunchKernelGGL((write_gemm_kernel<ST>), dim3(unsigned(L.count) * mtq * ntg * 8u), dim3(kGThreads), 0,
                        stream, p);
   } else {
     const size_t per_owner = size_t(L.d_ff) * (L.d_model / 4);
