@@ -42,12 +42,24 @@ def log(*a):
 KERNEL_SOURCES = ("rwttt_kernels.hip", "rwttt_device.h", "rwttt_kernels.h")
 
 
+def code_lines(text):
+    """The lines of a C/HIP source with // comments, blank lines and indentation removed."""
+    out = []
+    for line in text.splitlines():
+        code = line.split("//", 1)[0].strip()
+        if code:
+            out.append(code)
+    return out
+
+
 def kernel_source_sha():
-    """SHA-256 over the fast-weight kernel sources, in a fixed order."""
+    """SHA-256 over the code (comments dropped) of the fast-weight kernel sources, in a fixed order."""
     import hashlib
     h = hashlib.sha256()
     for name in KERNEL_SOURCES:
-        h.update(open(os.path.join(ROOT, "paper_2605_28053_amd", "csrc", name), "rb").read())
+        text = open(os.path.join(ROOT, "paper_2605_28053_amd", "csrc", name), encoding="utf-8").read()
+        h.update("\n".join(code_lines(text)).encode())
+        h.update(b"\0")
     return h.hexdigest()
 
 

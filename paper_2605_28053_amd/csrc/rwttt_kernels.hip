@@ -396,21 +396,22 @@ write_stream_kernel(const WriteParams p) {
 // copied as they are, 16 bytes per lane, by buffer loads that write LDS
 // directly (lane l of a load lands at LDS offset 16 l).  Ranks are consumed
 // in stages of 32 (A: 32 x 256 of Z, B: 32 x 128 of G, 24 KB), three stages
-// in flight; each wait names how many newer copies may still be outstanding.  The buffer range check turns every
-// 16-byte group outside the chunk or the matrix into zeros, so ragged tiles
-// need no other code.  The MFMA operands (8 consecutive ranks of one row m or
-// column n) are read back with the transposing LDS read ds_read_b64_tr_b16:
-// within each 16-lane group, lane i receives element i % 4 of the 8-byte runs
-// addressed by lanes 4j + i / 4, so lanes 4j + q address rank row j, columns
-// 4q..4q+3 and two such reads give one operand.  The 16-byte groups of rank
-// row r sit in slot (group ^ swz(r & 3)), swz = {0, 10, 4, 14}, chosen so
-// that every transposing read is free of bank conflicts.
+// in flight; each wait names how many newer copies may still be
+// outstanding.  The buffer range check turns every 16-byte group outside the
+// chunk or the matrix into zeros, so ragged tiles need no other code.  The
+// MFMA operands (8 consecutive ranks of one row m or column n) are read back
+// with the transposing LDS read ds_read_b64_tr_b16: within each 16-lane
+// group, lane i receives element i % 4 of the 8-byte runs addressed by lanes
+// 4j + i / 4, so lanes 4j + q address rank row j, columns 4q..4q+3 and two
+// such reads give one operand.  The 16-byte groups of rank row r sit in slot
+// (group ^ swz(r & 3)), swz = {0, 10, 4, 14}, chosen so that every
+// transposing read is free of bank conflicts.
 //
-// Epilogue: each wave passes its own accumulators through a private 8 KB LDS
-// region in 16-row steps (no block barrier), then reads back whole rows of
-// 8 columns per lane, adds eta * D to the live rows (prefetched one step
-// ahead) and stores the shadow rows, rounding to bf16 with the hardware
-// packed convert.
+// The MFMA is issued as D^T = G^T Z, so the accumulators of a lane hold runs
+// of four consecutive columns of one state row.  The epilogue combines them
+// with the live rows in that layout (bf16 state: live copied into the freed
+// stages; fp32 state: a register epilogue through a private LDS region) and
+// stores whole rows, rounding to bf16 with the hardware packed convert.
 
 constexpr int kGTM = 256;                                 // rows (d_ff) per tile
 constexpr int kGTN = 128;                                 // columns (d_model) per tile
