@@ -664,9 +664,11 @@ write_gemm_kernel(const WriteParams p) {
     const int scol = n0 + 8 * (lane & 15);
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
-      // half hf's copies are done once only what was issued after them is
-      // outstanding: the other half's 8 copies, or half 0's 8 stores
-      gemm_wait_vm<8>();
+      // half 0's copies are done once at most half 1's 8 copies are
+      // outstanding (loads complete in order); half 1's were waited for
+      // before any store was issued, since stores and loads may complete
+      // out of order relative to each other
+      if (hf == 0) gemm_wait_vm<8>();
       typedef __attribute__((address_space(3))) u32x2_t lds_u32x2_t;
       u32x2_t lt[4][4];
 #pragma unroll
@@ -687,6 +689,7 @@ write_gemm_kernel(const WriteParams p) {
               u32x2_t{bf16x2_rne(f0, f1), bf16x2_rne(f2, f3)};
         }
       asm volatile("" ::: "memory");
+      if (hf == 0) gemm_wait_vm<0>();
       const int row0 = m0 + wave * 64 + hf * 32;
       const int rows = max(0, min(32, p.d_ff - row0));
       const __amdgpu_buffer_rsrc_t sr = __builtin_amdgcn_make_buffer_rsrc(
