@@ -117,6 +117,8 @@ WRITE_CASES = [
     (1000, 264, "bf16", "f32", 17, [0, 3, 1]),
     (1000, 264, "bf16", "bf16", 64, [1, 2]),
     (520, 1032, "bf16", "f32", 100, [3, 0]),
+    (264, 136, "bf16", "bf16", 150, [0, 2]),           # GEMM with 5 rank stages (last stage index 1 of 3)
+    (520, 264, "bf16", "f32", 150, [1]),
     (128, 64, "bf16", "f32", 32, [0, 1, 2, 3]),
     (9728, 2560, "bf16", "f32", 64, [1]),
 ]
@@ -546,11 +548,12 @@ def test_read_bf16_output_rounding_is_exact():
         assert np.array_equal(to_host(y[r], "bf16"), want), r
 
 
-@pytest.mark.parametrize("chunk", [1, 128])
+@pytest.mark.parametrize("chunk", [1, 128, 150, 170])
 def test_write_bf16_state_rounding_is_exact(chunk):
     """live + 1.0 * Z^T G with one unit rank is an exact fp32 sum; the bf16 shadow must be RNE.
 
-    chunk 1 takes the streaming WRITE kernel, chunk 128 the GEMM kernel.
+    chunk 1 takes the streaming WRITE kernel, the others the GEMM kernel, whose last rank stage
+    then sits in each of its three LDS stages in turn (4, 5 and 6 stages of 32 ranks).
     """
     d_ff, d_model = 256, 512
     wl = small_workload(d_ff, d_model, "bf16", "bf16", 1, eta=1.0)
