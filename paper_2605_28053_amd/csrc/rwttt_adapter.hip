@@ -20,9 +20,10 @@ namespace {
 
 constexpr int kAThreads = 1024;   // READ partial blocks: 16 waves share one chunk of rows
 constexpr int kAWaves = kAThreads / 64;
-constexpr int kAChunk = 256;      // K rows per READ work item
+constexpr int kAChunk = 192;      // K rows per READ work item
 constexpr int kAUnroll = 4;
 constexpr int kAGroup = 8;        // owners per READ block: W0 is read once for all of them
+constexpr int kARedCols = 64;     // READ reduce: columns per block (four waves split the chunks)
 constexpr int kAPQRows = 64;      // evidence rows of P or Q staged per pass of the update
 
 // ---------------------------------------------------------------------------
@@ -41,8 +42,9 @@ constexpr int kAPQRows = 64;      // evidence rows of P or Q staged per pass of 
 //    g mod (tiles), and the first tile's block appends the x chunk to the
 //    owners' tails if asked.
 // 2. adapter_read_reduce_kernel: u = sum of the chunks' shares in chunk
-//    order; y[n] = (sum of the W0 partials in chunk order) + sum_j u[j] B[j][n],
-//    rounded once to the io dtype.
+//    order; y[n] = (sum of the W0 partials: four contiguous quarters of the
+//    chunks, each in chunk order, then the quarters in order) +
+//    sum_j u[j] B[j][n], rounded once to the io dtype.
 
 struct AReadParams {
   const void* x;
@@ -62,7 +64,7 @@ __global__ void __launch_bounds__(kAThreads) adapter_read_partial_kernel(const A
   constexpr int TILE_N = 64 * COLS;
   constexpr int RW = kAChunk / kAWaves;
   __shared__ float xs[kAGroup][kAChunk];
-  __shared__ float red[kAWaves][TILE_N];
+  __shared__ float red[4][kAWaves][TILE_N];
   __shared__ float ured[kAChunk * 8];
   __shared__ float useg[(kAChunk / 8) * 8];
 
@@ -86,6 +88,17 @@ __global__ void __launch_bounds__(kAThreads) adapter_read_partial_kernel(const A
   const int b0 = gi * kAGroup;
   const int ng = min(kAGroup, p.count - b0);
 
+  // this wave's first round of W0 rows is requested before the x staging
+  const int kw0 = wave * RW;
+  const int kw1 = min(kw0 + RW, kn);
+  const IO* wbase = static_cast<const IO*>(p.w0) + size_t(k0) * p.d_model + col;
+  Packed<IO, COLS> w[kAUnroll];
+#pragma unroll
+  for (int u = 0; u < kAUnroll; ++u) {
+    if (col_ok && kw0 + u < kw1) load_packed<false>(wbase + size_t(kw0 + u) * p.d_model, w[u]);
+    else w[u].zero();
+  }
+
   for (int idx = tid; idx < kAGroup * kAChunk; idx += kAThreads) {
     const int g = idx / kAChunk, k = idx - g * kAChunk;
     xs[g][k] = (g < ng && k < kn)
@@ -102,21 +115,19 @@ __global__ void __launch_bounds__(kAThreads) adapter_read_partial_kernel(const A
   __syncthreads();
 
   // x W0 over this wave's rows for every owner of the group: W0 is read once
-  const int kw0 = wave * RW;
-  const int kw1 = min(kw0 + RW, kn);
   float acc[kAGroup][COLS];
 #pragma unroll
   for (int g = 0; g < kAGroup; ++g)
 #pragma unroll
     for (int c = 0; c < COLS; ++c) acc[g][c] = 0.f;
   if (col_ok) {
-    const IO* wbase = static_cast<const IO*>(p.w0) + size_t(k0) * p.d_model + col;
     for (int k = kw0; k < kw1; k += kAUnroll) {
-      Packed<IO, COLS> w[kAUnroll];
+      if (k != kw0) {
 #pragma unroll
-      for (int u = 0; u < kAUnroll; ++u) {
-        if (k + u < kw1) load_packed<false>(wbase + size_t(k + u) * p.d_model, w[u]);
-        else w[u].zero();
+        for (int u = 0; u < kAUnroll; ++u) {
+          if (k + u < kw1) load_packed<false>(wbase + size_t(k + u) * p.d_model, w[u]);
+          else w[u].zero();
+        }
       }
 #pragma unroll
       for (int u = 0; u < kAUnroll; ++u) {
@@ -129,19 +140,24 @@ __global__ void __launch_bounds__(kAThreads) adapter_read_partial_kernel(const A
       }
     }
   }
-  // per owner: the waves' sums in wave order -> one partial per (owner, chunk, tile)
+  // per owner: the waves' sums in wave order -> one partial per (owner, chunk,
+  // tile); four owners per pass through LDS
 #pragma unroll
-  for (int g = 0; g < kAGroup; ++g) {
-    if (g < ng) {
+  for (int g0 = 0; g0 < kAGroup; g0 += 4) {
+    if (g0 < ng) {
 #pragma unroll
-      for (int c = 0; c < COLS; ++c) red[wave][lane * COLS + c] = acc[g][c];
+      for (int gg = 0; gg < 4; ++gg)
+#pragma unroll
+        for (int c = 0; c < COLS; ++c) red[gg][wave][lane * COLS + c] = acc[g0 + gg][c];
       __syncthreads();
-      float* dst = p.part + (size_t(p.row[b0 + g]) * p.ks + kc) * p.npad + nt * TILE_N;
-      for (int j = tid; j < TILE_N; j += kAThreads) {
-        float v = red[0][j];
+      for (int idx = tid; idx < 4 * TILE_N; idx += kAThreads) {
+        const int gg = idx / TILE_N, j = idx - gg * TILE_N;
+        if (g0 + gg < ng) {
+          float v = red[gg][0][j];
 #pragma unroll
-        for (int w = 1; w < kAWaves; ++w) v += red[w][j];
-        dst[j] = v;
+          for (int w = 1; w < kAWaves; ++w) v += red[gg][w][j];
+          p.part[(size_t(p.row[b0 + g0 + gg]) * p.ks + kc) * p.npad + nt * TILE_N + j] = v;
+        }
       }
       __syncthreads();
     }
@@ -186,15 +202,22 @@ __global__ void __launch_bounds__(256) adapter_read_reduce_kernel(const AReadPar
   __shared__ float us[8][RWTTT_MAX_RANK];
   __shared__ float u[RWTTT_MAX_RANK];
   const int b = blockIdx.y;
-  const int n = blockIdx.x * 256 + threadIdx.x;
+  const int n = blockIdx.x * kARedCols + (threadIdx.x & 63);
   const size_t r = p.row[b];
   {
     // u[j] = sum over chunks of the x A shares: eight strided partial sums per
     // rank column, then those eight in order
     const int j = threadIdx.x & 31, q = threadIdx.x >> 5;
     if (j < p.rank) {
+      // chunks q, q + 8, q + 16, ... in order; eight loads in flight at a time
       float s = 0.f;
-      for (int kc = q; kc < p.ks; kc += 8) s += p.upart[(r * p.ks + kc) * p.rank + j];
+      for (int kc = q; kc < p.ks; kc += 64) {
+        float a[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) a[i] = kc + 8 * i < p.ks ? p.upart[(r * p.ks + kc + 8 * i) * p.rank + j] : 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s += a[i];
+      }
       us[q][j] = s;
     }
     __syncthreads();
@@ -206,22 +229,37 @@ __global__ void __launch_bounds__(256) adapter_read_reduce_kernel(const AReadPar
     }
     __syncthreads();
   }
-  if (n >= p.d_model) return;
-  const float* q = p.part + r * p.ks * p.npad + n;
+  // W0 partials: the four waves sum four contiguous quarters of the chunks,
+  // each in chunk order, and the quarters are added in order
+  __shared__ float qs[4][kARedCols];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int per = (p.ks + 3) / 4;
+  const int k0 = wave * per, k1 = min(p.ks, k0 + per);
   float s = 0.f;
-  int kc = 0;
-  for (; kc + 8 <= p.ks; kc += 8) {
-    float a[8];
+  if (n < p.d_model) {
+    const float* q = p.part + r * p.ks * p.npad + n;
+    for (int kc = k0; kc < k1; kc += 8) {
+      float a[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) a[i] = q[size_t(kc + i) * p.npad];
+      for (int i = 0; i < 8; ++i) a[i] = kc + i < k1 ? q[size_t(kc + i) * p.npad] : 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) s += a[i];
+      for (int i = 0; i < 8; ++i) s += a[i];
+    }
   }
-  for (; kc < p.ks; ++kc) s += q[size_t(kc) * p.npad];
+  qs[wave][lane] = s;
+  __syncthreads();
+  if (wave != 0 || n >= p.d_model) return;
   const ST* Bm = static_cast<const ST*>(p.state[b]) + size_t(p.d_ff) * p.rank;
   float lr = 0.f;
-  for (int j = 0; j < p.rank; ++j) lr = fmaf(u[j], Elem<ST>::get(Bm, size_t(j) * p.d_model + n), lr);
-  Elem<IO>::put(p.y, r * p.d_model + n, s + lr);
+  for (int j0 = 0; j0 < p.rank; j0 += 8) {
+    float bv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) bv[i] = j0 + i < p.rank ? Elem<ST>::get(Bm, size_t(j0 + i) * p.d_model + n) : 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (j0 + i < p.rank) lr = fmaf(u[j0 + i], bv[i], lr);
+  }
+  Elem<IO>::put(p.y, r * p.d_model + n, (((qs[0][lane] + qs[1][lane]) + qs[2][lane]) + qs[3][lane]) + lr);
 }
 
 // ---------------------------------------------------------------------------
@@ -393,7 +431,7 @@ hipError_t launch_adapter_read_t(const AdapterReadLaunch& L, hipStream_t stream)
   const unsigned groups = unsigned((L.count + kAGroup - 1) / kAGroup);
   hipLaunchKernelGGL((adapter_read_partial_kernel<IO, ST>), dim3(pairs8 * groups),
                      dim3(kAThreads), 0, stream, p);
-  hipLaunchKernelGGL((adapter_read_reduce_kernel<IO, ST>), dim3((L.d_model + 255) / 256, L.count),
+  hipLaunchKernelGGL((adapter_read_reduce_kernel<IO, ST>), dim3((L.d_model + kARedCols - 1) / kARedCols, L.count),
                      dim3(256), 0, stream, p);
   return hipGetLastError();
 }
