@@ -221,7 +221,7 @@ __global__ void __launch_bounds__(256) adapter_read_reduce_kernel(const AReadPar
       us[q][j] = s;
     }
     __syncthreads();
-    if (threadIdx.x < p.rank) {
+    if (int(threadIdx.x) < p.rank) {
       float s = 0.f;
 #pragma unroll
       for (int i = 0; i < 8; ++i) s += us[i][threadIdx.x];

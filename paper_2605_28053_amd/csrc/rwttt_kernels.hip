@@ -518,8 +518,8 @@ write_gemm_kernel(const WriteParams p) {
   uint32_t voff[kGCopies];
 #pragma unroll
   for (int t = 0; t < kGCopies; ++t) {
-    const bool za = t < 4;
-    const int u = wave + 4 * (za ? t : t - 4);
+    const bool za = t < kGUnitsA / 4;
+    const int u = wave + 4 * (za ? t : t - kGUnitsA / 4);
     const int r = za ? 2 * u + (lane >> 5) : 4 * u + (lane >> 4);
     const int s = za ? (lane & 31) : (lane & 15);
     const int col = (za ? m0 : n0) + 8 * (s ^ gemm_swz(r));
@@ -533,8 +533,8 @@ write_gemm_kernel(const WriteParams p) {
     const i32x4_t gr = gemm_rsrc(G + size_t(c0) * p.d_model, rows * p.d_model * 2);
 #pragma unroll
     for (int t = 0; t < kGCopies; ++t) {
-      const bool za = t < 4;
-      const int u = wave + 4 * (za ? t : t - 4);
+      const bool za = t < kGUnitsA / 4;
+      const int u = wave + 4 * (za ? t : t - kGUnitsA / 4);
       gemm_copy(st + (za ? 0 : kGStageA) + u * 512, voff[t], za ? zr : gr);
     }
   };
