@@ -63,12 +63,14 @@ def kernel_source_sha():
     return h.hexdigest()
 
 
-def measured_traffic(records):
+def measured_traffic(records, wl):
     """Mean HBM bytes per READ call from the committed rocprofv3 PMC summary.
 
     The summary holds FETCH_SIZE and WRITE_SIZE per dispatch, scaled by what
-    the same counters read for a plain 1 GiB device copy.  It is used only if
-    the kernel source is the one the counters were taken on; else None.
+    the same counters read for a plain 1 GiB device copy, per READ group size
+    at one shape.  It is used only if the kernel source is the one the
+    counters were taken on and the workload's READ has that shape and every
+    group size in the table; else None.
     """
     path = os.path.join(ROOT, "profiles", "hbm_traffic__mixed8-4b-36L.json")
     try:
@@ -77,6 +79,9 @@ def measured_traffic(records):
     except OSError:
         return None
     if summ.get("kernel_source_sha256") != sha:
+        return None
+    shape = {"d_model": wl.d_model, "d_ff": wl.d_ff, "io": wl.io_dtype, "state": wl.state_dtype}
+    if summ.get("read_shape") != shape:
         return None
     table = summ["read_call_bytes_by_group_size"]
     tot, calls = 0.0, 0
@@ -326,6 +331,43 @@ def run_cpu_baseline(args, wl, kept):
                         f"{dt:.2f} s measured, scaled x{scale:g} to all layers"))
 
 
+def time_library_write(torch, wl, wr, calls=20):
+    """The same update as the commonest WRITE call, shadow = live + eta * Z^T G, as one
+    torch.baddbmm over the call's owners (bf16 operands and state, fp32 accumulate in
+    the library), on fresh seeded tensors of the workload's distributions.  Context
+    for the WRITE kernel's figure only: no step of the measured path runs here."""
+    if wl.state_dtype != "bf16":
+        return {"skipped": "the library update needs one dtype for state and operands; "
+                           f"this workload's state is {wl.state_dtype}"}
+    counts = {}
+    for _, b, c, _, _, n in wr["records"]:
+        counts[(b, c)] = counts.get((b, c), 0) + n
+    (b, c), _ = max(counts.items(), key=lambda kv: kv[1])
+    K, N = wl.d_ff, wl.d_model
+    gen = torch.Generator(device="cuda").manual_seed(0)
+    bf = torch.bfloat16
+    zt = torch.randn(b, c, K, device="cuda", dtype=bf, generator=gen).abs_().transpose(1, 2).contiguous()
+    g = torch.randn(b, c, N, device="cuda", dtype=bf, generator=gen)
+    live = torch.randn(b, K, N, device="cuda", dtype=bf, generator=gen).mul_(0.02)
+    out = torch.empty_like(live)
+    for _ in range(3):
+        torch.baddbmm(live, zt, g, alpha=wl.eta, out=out)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(calls):
+        torch.baddbmm(live, zt, g, alpha=wl.eta, out=out)
+    e1.record()
+    torch.cuda.synchronize()
+    us = 1e3 * e0.elapsed_time(e1) / calls
+    flop = 2.0 * b * c * K * N
+    return {"op": "torch.baddbmm(live, Z^T, G, alpha=eta), bf16, out of place",
+            "owners": b, "chunk": c, "calls": calls, "avg_us": round(us, 2),
+            "tflops": round(flop / us / 1e6, 1),
+            "mfma_frac": round(flop / us / 1e6 / BF16_MFMA_PEAK_TFLOPS, 4),
+            "this_write_avg_us": round(wr["avg_us"], 2)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -344,6 +386,9 @@ def main():
                     help="2 (default): mixed8-4b-36L; 1 read8-4b; 3 ragged32-4b; 4 prefill8-8b")
     ap.add_argument("--rank", type=int, default=0,
                     help="0: fast-weight state (default); r > 0: the rank-r adapter backend")
+    ap.add_argument("--library-write", choices=["on", "off"], default="off",
+                    help="also time torch.baddbmm (the vendor GEMM library) on the same "
+                         "update as one WRITE call, for a bf16 state (context, not the value)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run 5 plain device copies of BYTES each (HBM counter calibration)")
     args = ap.parse_args()
@@ -406,7 +451,7 @@ def main():
     }
     if "read" in kern:
         rd = kern["read"]
-        traffic = None if args.rank else measured_traffic(rd["records"])
+        traffic = None if args.rank else measured_traffic(rd["records"], wl)
         line["roofline"] = {"bound": "hbm",
                             "kernel": ("adapter_read_partial_kernel+adapter_read_reduce_kernel"
                                        if args.rank else "read_partial_kernel+read_reduce_kernel"),
@@ -429,6 +474,8 @@ def main():
                                 "achieved_tflops": round(wr["tflops"], 2),
                                 "mfma_frac": round(wr["tflops"] / BF16_MFMA_PEAK_TFLOPS, 5),
                                 "avg_launch_us": round(wr["avg_us"], 2), "launches": wr["launches"]}
+    if args.library_write == "on" and wkind in kern:
+        line["library_write"] = time_library_write(torch, wl, kern[wkind])
     if args.cpu_baseline == "on":
         line["cpu_baseline"] = run_cpu_baseline(args, wl, g["kept"])
     line["paper_context"] = ("274.61 tok/s, 9.31x over sequential serving: full Qwen3-4B "

@@ -247,6 +247,23 @@ def test_bench_refuses_more_than_one_gpu():
     assert "one GPU" in r.stderr
 
 
+def test_bench_traffic_applies_only_to_its_shape_and_source():
+    """The PMC traffic table is reported only for the READ shape, group sizes and
+    kernel source it was measured on."""
+    import bench
+    from rwttt_inputs import workload
+    rec = lambda b, n: ("read", b, 0, None, None, n)
+    mixed, prefill, ragged = workload(2), workload(4), workload(3)
+    t = bench.measured_traffic([rec(8, 3), rec(7, 1)], mixed)
+    assert t is not None and 7e8 < t < 9e8
+    assert bench.measured_traffic([rec(8, 1)], prefill) is None
+    assert bench.measured_traffic([rec(16, 1)], ragged) is None
+    # comments and indentation do not change the key, code does
+    code = "int a; // x\n  int b;\n\n"
+    assert bench.code_lines(code) == ["int a;", "int b;"]
+    assert bench.code_lines("int a; // y\nint b;") == bench.code_lines(code)
+
+
 def test_plain_c_client_builds_against_the_header_and_runs(tmp_path):
     """The header is C (not only C++): a C11 client compiles with gcc, links the
     library and drives planning and the owner table on a host-only context."""
