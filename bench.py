@@ -360,11 +360,22 @@ def time_library_write(torch, wl, wr, calls=20):
     e1.record()
     torch.cuda.synchronize()
     us = 1e3 * e0.elapsed_time(e1) / calls
+    # the bare product with a bf16 result: no live term, the same bytes written
+    for _ in range(3):
+        torch.bmm(zt, g, out=out)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(calls):
+        torch.bmm(zt, g, out=out)
+    e1.record()
+    torch.cuda.synchronize()
+    us_bmm = 1e3 * e0.elapsed_time(e1) / calls
     flop = 2.0 * b * c * K * N
     return {"op": "torch.baddbmm(live, Z^T, G, alpha=eta), bf16, out of place",
             "owners": b, "chunk": c, "calls": calls, "avg_us": round(us, 2),
             "tflops": round(flop / us / 1e6, 1),
             "mfma_frac": round(flop / us / 1e6 / BF16_MFMA_PEAK_TFLOPS, 4),
+            "bmm_without_live_avg_us": round(us_bmm, 2),
             "this_write_avg_us": round(wr["avg_us"], 2)}
 
 

@@ -18,29 +18,58 @@ namespace {
 
 #include "rwttt_device.h"
 
-constexpr int kAThreads = 1024;   // READ partial blocks: 16 waves share one chunk of rows
+constexpr int kAThreads = 512;    // READ partial blocks: 8 waves, two per SIMD
 constexpr int kAWaves = kAThreads / 64;
 constexpr int kAChunk = 192;      // K rows per READ work item
-constexpr int kAUnroll = 4;
+constexpr int kARows = kAChunk / kAWaves;   // W0 rows per wave, all requested at once
 constexpr int kAGroup = 8;        // owners per READ block: W0 is read once for all of them
+constexpr int kAURows = kAChunk / 64;   // chunk rows per lane in the u share
 constexpr int kARedCols = 64;     // READ reduce: columns per block (four waves split the chunks)
+constexpr int kARedLoads = 16;    // READ reduce: partials in flight per lane
 constexpr int kAPQRows = 64;      // evidence rows of P or Q staged per pass of the update
+
+__device__ __forceinline__ float to_f32(float v) { return v; }
+__device__ __forceinline__ float to_f32(uint16_t v) { return __uint_as_float(uint32_t(v) << 16); }
+
+// x.lo * w.lo + x.hi * w.hi + acc over packed bf16 pairs (v_dot2c_f32_bf16)
+__device__ __forceinline__ float dot2_bf16(uint32_t x, uint32_t w, float acc) {
+  typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_v, x), __builtin_bit_cast(bf16x2_v, w),
+                                         acc, false);
+}
+
+// An empty asm that reads and rewrites four or eight accumulators: the
+// arithmetic that produced them cannot move past it.
+__device__ __forceinline__ void pin_row(float (&a)[4]) {
+  asm volatile("" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]));
+}
+__device__ __forceinline__ void pin_row(float (&a)[8]) {
+  asm volatile("" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(a[4]), "+v"(a[5]),
+               "+v"(a[6]), "+v"(a[7]));
+}
+
+// Barrier for data exchanged through LDS: this wave's LDS accesses are
+// complete, global loads stay in flight (the compiler waits for those where
+// their registers are used).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 // ---------------------------------------------------------------------------
 // READ
 // ---------------------------------------------------------------------------
 //
-// 1. adapter_read_partial_kernel: one 1024-thread block per (K chunk of 256
+// 1. adapter_read_partial_kernel: one 512-thread block per (K chunk of 192
 //    rows, column tile, group of up to 8 owners); each lane streams 16 bytes
 //    of every W0 row of the tile once and applies it to all the block's
-//    owners, the sixteen waves split the chunk's rows (16 each: four rounds of
-//    four loads per wave), and each owner's wave sums
-//    are added in wave order into one partial per (owner, chunk, tile).  Owner groups of
-//    one (chunk, tile) sit on one XCD (dispatch is round-robin over the 8
-//    XCDs).  The chunk's tile blocks also form the owners' chunk shares of
-//    u = x A (r values each, ordered two-level sums), owner g in tile
-//    g mod (tiles), and the first tile's block appends the x chunk to the
-//    owners' tails if asked.
+//    owners.  The eight waves split the chunk's rows, 24 each, and request all
+//    of them before any arithmetic (after the x chunk, so that staging x does
+//    not wait for W0).  Each owner's wave sums are added in wave order into
+//    one partial per (owner, chunk, tile).  Owner groups of one (chunk, tile)
+//    sit on one XCD (dispatch is round-robin over the 8 XCDs).  The chunk's
+//    tile blocks also form the owners' chunk shares of u = x A (r values
+//    each, ordered two-level sums), owner g in tile g mod (tiles), and the
+//    first tile's block appends the x chunk to the owners' tails if asked.
 // 2. adapter_read_reduce_kernel: u = sum of the chunks' shares in chunk
 //    order; y[n] = (sum of the W0 partials: four contiguous quarters of the
 //    chunks, each in chunk order, then the quarters in order) +
@@ -59,18 +88,18 @@ struct AReadParams {
 };
 
 template <typename IO, typename ST>
-__global__ void __launch_bounds__(kAThreads) adapter_read_partial_kernel(const AReadParams p) {
+__global__ void __launch_bounds__(kAThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+adapter_read_partial_kernel(const AReadParams p) {
   constexpr int COLS = 16 / sizeof(IO);
   constexpr int TILE_N = 64 * COLS;
-  constexpr int RW = kAChunk / kAWaves;
-  __shared__ float xs[kAGroup][kAChunk];
-  __shared__ float red[4][kAWaves][TILE_N];
-  __shared__ float ured[kAChunk * 8];
-  __shared__ float useg[(kAChunk / 8) * 8];
+  __shared__ float xs[kAChunk][kAGroup];   // x chunk, row-major over owners
+  // bf16 io: the same chunk as raw bf16, rows 2m and 2m + 1 of an owner in one word
+  __shared__ uint16_t xh[sizeof(IO) == 2 ? kAChunk / 2 : 1][kAGroup][2];
+  __shared__ float red[kAGroup][kAWaves][TILE_N];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar indexing
   // block -> (XCD, position) -> ((chunk, tile) pair, owner group)
   const int ngroups = (p.count + kAGroup - 1) / kAGroup;
   const int xcd = blockIdx.x & 7;
@@ -88,111 +117,183 @@ __global__ void __launch_bounds__(kAThreads) adapter_read_partial_kernel(const A
   const int b0 = gi * kAGroup;
   const int ng = min(kAGroup, p.count - b0);
 
-  // this wave's first round of W0 rows is requested before the x staging
-  const int kw0 = wave * RW;
-  const int kw1 = min(kw0 + RW, kn);
-  const IO* wbase = static_cast<const IO*>(p.w0) + size_t(k0) * p.d_model + col;
-  Packed<IO, COLS> w[kAUnroll];
+  // 1. requests, in the order they are needed: the x chunk and the first eight
+  //    A columns of the rows this lane takes in the u share; once x is staged,
+  //    this wave's W0 rows.  Every request is unconditional (indices clamped into
+  //    the buffers, unused values zeroed afterwards) so that no load waits
+  //    inside a branch.
+  uint32_t rows[kAGroup];   // owner rows of the group's slots (block-uniform)
 #pragma unroll
-  for (int u = 0; u < kAUnroll; ++u) {
-    if (col_ok && kw0 + u < kw1) load_packed<false>(wbase + size_t(kw0 + u) * p.d_model, w[u]);
-    else w[u].zero();
-  }
-
-  for (int idx = tid; idx < kAGroup * kAChunk; idx += kAThreads) {
+  for (int g = 0; g < kAGroup; ++g) rows[g] = p.row[b0 + min(g, ng - 1)];
+  constexpr int XPER = kAGroup * kAChunk / kAThreads;
+  IO xv[XPER];   // raw until staged
+#pragma unroll
+  for (int i = 0; i < XPER; ++i) {
+    const int idx = tid + i * kAThreads;
     const int g = idx / kAChunk, k = idx - g * kAChunk;
-    xs[g][k] = (g < ng && k < kn)
-                   ? Elem<IO>::get(p.x, size_t(p.row[b0 + g]) * p.d_ff + k0 + k) : 0.f;
+    uint32_t r = rows[0];
+#pragma unroll
+    for (int g2 = 1; g2 < kAGroup; ++g2) r = g == g2 ? rows[g2] : r;
+    xv[i] = static_cast<const IO*>(p.x)[size_t(r) * p.d_ff + k0 + min(k, kn - 1)];
   }
-  if (nt == 0) {
-    for (int g = 0; g < ng; ++g) {
-      if (p.tail[b0 + g] == nullptr) continue;
-      const IO* xr = static_cast<const IO*>(p.x) + size_t(p.row[b0 + g]) * p.d_ff + k0;
-      IO* tr = static_cast<IO*>(p.tail[b0 + g]) + k0;
-      for (int k = tid; k < kn; k += kAThreads) tr[k] = xr[k];
+  asm volatile("" ::: "memory");   // requests leave in this order
+  // u share (step 2): wave i takes owner nt + i * tiles of the group; its lanes
+  // hold rows lane, lane + 64, lane + 128 of the chunk.  Their first eight A
+  // columns are requested here, by the waves that have an owner.
+  const int ug = nt + wave * p.nt;
+  const ST* uA = static_cast<const ST*>(p.state[b0 + (ug < ng ? ug : 0)]);
+  float apre[kAURows][8];
+  if (ug < ng) {
+#pragma unroll
+    for (int r = 0; r < kAURows; ++r) {
+      const size_t at = size_t(k0 + min(lane + 64 * r, kn - 1)) * p.rank;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) apre[r][j] = Elem<ST>::get(uA, at + min(j, p.rank - 1));
     }
+  } else {
+#pragma unroll
+    for (int r = 0; r < kAURows; ++r)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) apre[r][j] = 0.f;
   }
-  __syncthreads();
+  __builtin_amdgcn_sched_barrier(0);   // x is waited for only after the A requests are out
+  // the x chunk is staged before the W0 rows are requested: under the W0
+  // stream its few loads would come back last
+#pragma unroll
+  for (int i = 0; i < XPER; ++i) {
+    const int idx = tid + i * kAThreads;
+    const int g = idx / kAChunk, k = idx - g * kAChunk;
+    const bool ok = g < ng && k < kn;
+    xs[k][g] = ok ? to_f32(xv[i]) : 0.f;
+    if constexpr (sizeof(IO) == 2) xh[k >> 1][g][k & 1] = ok ? xv[i] : uint16_t(0);
+  }
+  lds_barrier();
+  // rows past the chunk repeat its last row (their x is zero); lanes past
+  // d_model read column 0 and their sums are dropped
+  const int kw0 = wave * kARows;
+  const IO* wbase = static_cast<const IO*>(p.w0) + size_t(k0) * p.d_model + (col_ok ? col : 0);
+  Packed<IO, COLS> w[kARows];
+#pragma unroll
+  for (int u = 0; u < kARows; ++u)
+    load_packed<false>(wbase + size_t(min(kw0 + u, kn - 1)) * p.d_model, w[u]);
+  __builtin_amdgcn_sched_barrier(0);   // every W0 request is out before any arithmetic
 
-  // x W0 over this wave's rows for every owner of the group: W0 is read once
+  // 2. u share of this chunk for the wave's owner: sum_k x[k] A[k][j], eight
+  //    rank columns per pass: each lane sums its rows in order, then a
+  //    butterfly over the wave (every lane ends with the same sum).  The first
+  //    pass uses the requested columns and runs while the W0 rows are still
+  //    arriving; passes for ranks above eight load theirs at the end.
+  float* ur = p.upart + (size_t(p.row[b0 + (ug < ng ? ug : 0)]) * p.ks + kc) * p.rank;
+  auto u_pass = [&](int j0, bool loaded) {
+    float sj[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sj[j] = 0.f;
+#pragma unroll
+    for (int r = 0; r < kAURows; ++r) {
+      const int k = lane + 64 * r;
+      const float xk = xs[k][ug];   // zero past the chunk
+      const size_t at = size_t(k0 + min(k, kn - 1)) * p.rank;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float a = loaded ? apre[r][j] : Elem<ST>::get(uA, at + min(j0 + j, p.rank - 1));
+        sj[j] = fmaf(xk, j0 + j < p.rank ? a : 0.f, sj[j]);
+      }
+    }
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) sj[j] += __shfl_xor(sj[j], m);
+    float v = sj[0];
+#pragma unroll
+    for (int j = 1; j < 8; ++j) v = lane == j ? sj[j] : v;
+    if (lane < 8 && j0 + lane < p.rank) ur[j0 + lane] = v;
+  };
+  if (ug < ng) u_pass(0, true);
+
+  // 3. x W0 over this wave's rows for every owner of the group, rows in order
   float acc[kAGroup][COLS];
 #pragma unroll
   for (int g = 0; g < kAGroup; ++g)
 #pragma unroll
     for (int c = 0; c < COLS; ++c) acc[g][c] = 0.f;
-  if (col_ok) {
-    for (int k = kw0; k < kw1; k += kAUnroll) {
-      if (k != kw0) {
+  if constexpr (sizeof(IO) == 2) {
+    // bf16: rows in pairs, one v_dot2 per (owner, column) adds
+    // x[2m] W[2m][c] + x[2m+1] W[2m+1][c]; v_perm pairs the two rows' values
+    // of a column in one word
 #pragma unroll
-        for (int u = 0; u < kAUnroll; ++u) {
-          if (k + u < kw1) load_packed<false>(wbase + size_t(k + u) * p.d_model, w[u]);
-          else w[u].zero();
-        }
-      }
+    for (int m = 0; m < kARows / 2; ++m) {
+      const uint32_t* xq = reinterpret_cast<const uint32_t*>(&xh[(kw0 >> 1) + m][0][0]);
+      const uint4 xa = *reinterpret_cast<const uint4*>(xq);
+      const uint4 xb = *reinterpret_cast<const uint4*>(xq + 4);
+      const uint32_t xpair[kAGroup] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
 #pragma unroll
-      for (int u = 0; u < kAUnroll; ++u) {
+      for (int i = 0; i < COLS / 2; ++i) {
+        const uint32_t lo = __builtin_amdgcn_perm(w[2 * m + 1].w[i], w[2 * m].w[i], 0x05040100u);
+        const uint32_t hi = __builtin_amdgcn_perm(w[2 * m + 1].w[i], w[2 * m].w[i], 0x07060302u);
 #pragma unroll
         for (int g = 0; g < kAGroup; ++g) {
-          const float xv = xs[g][k + u];
-#pragma unroll
-          for (int c = 0; c < COLS; ++c) acc[g][c] = fmaf(xv, w[u].get(c), acc[g][c]);
+          acc[g][2 * i] = dot2_bf16(xpair[g], lo, acc[g][2 * i]);
+          acc[g][2 * i + 1] = dot2_bf16(xpair[g], hi, acc[g][2 * i + 1]);
         }
       }
+      // one row pair at a time: its x values and paired W0 die before the next
+#pragma unroll
+      for (int g = 0; g < kAGroup; ++g) pin_row(acc[g]);
     }
-  }
-  // per owner: the waves' sums in wave order -> one partial per (owner, chunk,
-  // tile); four owners per pass through LDS
+  } else {
 #pragma unroll
-  for (int g0 = 0; g0 < kAGroup; g0 += 4) {
-    if (g0 < ng) {
+    for (int u = 0; u < kARows; ++u) {
+      float xr[kAGroup];
 #pragma unroll
-      for (int gg = 0; gg < 4; ++gg)
-#pragma unroll
-        for (int c = 0; c < COLS; ++c) red[gg][wave][lane * COLS + c] = acc[g0 + gg][c];
-      __syncthreads();
-      for (int idx = tid; idx < 4 * TILE_N; idx += kAThreads) {
-        const int gg = idx / TILE_N, j = idx - gg * TILE_N;
-        if (g0 + gg < ng) {
-          float v = red[gg][0][j];
-#pragma unroll
-          for (int w = 1; w < kAWaves; ++w) v += red[gg][w][j];
-          p.part[(size_t(p.row[b0 + g0 + gg]) * p.ks + kc) * p.npad + nt * TILE_N + j] = v;
-        }
+      for (int g = 0; g < kAGroup; g += 4) {
+        const float4 x4 = *reinterpret_cast<const float4*>(&xs[kw0 + u][g]);
+        xr[g] = x4.x; xr[g + 1] = x4.y; xr[g + 2] = x4.z; xr[g + 3] = x4.w;
       }
-      __syncthreads();
+#pragma unroll
+      for (int g = 0; g < kAGroup; ++g)
+#pragma unroll
+        for (int c = 0; c < COLS; ++c) acc[g][c] = fmaf(xr[g], w[u].get(c), acc[g][c]);
+      // one row at a time: the row's products are done here, so its x values
+      // and converted W0 die before the next row's are formed
+#pragma unroll
+      for (int g = 0; g < kAGroup; ++g) pin_row(acc[g]);
     }
   }
 
-  // u share of this chunk for each owner: sum_k x[k] A[k][j], eight rank columns
-  // per pass; the chunk's column-tile blocks take the owners in turn (the loop
-  // bounds are uniform per block, so every barrier is reached by all threads)
-  for (int g = nt; g < ng; g += p.nt) {
-    const ST* A = static_cast<const ST*>(p.state[b0 + g]);
-    float* ur = p.upart + (size_t(p.row[b0 + g]) * p.ks + kc) * p.rank;
-    for (int j0 = 0; j0 < p.rank; j0 += 8) {
-      const int k = tid;   // one chunk row per thread of the first 256
-      if (k < kAChunk) {
+  // 4. per owner: the waves' sums in wave order -> one partial per (owner,
+  //    chunk, tile), all owners in one pass through LDS
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const bool ok = k < kn && j0 + j < p.rank;
-          ured[k * 8 + j] = ok ? xs[g][k] * Elem<ST>::get(A, size_t(k0 + k) * p.rank + j0 + j) : 0.f;
-        }
-      }
-      __syncthreads();
-      if (tid < kAChunk) {
-        const int j = tid & 7, seg = tid >> 3;   // 32 segments of 8 rows
-        float s = 0.f;
+  for (int g = 0; g < kAGroup; ++g)
 #pragma unroll
-        for (int i = 0; i < 8; ++i) s += ured[(seg * 8 + i) * 8 + j];
-        useg[seg * 8 + j] = s;
+    for (int c = 0; c < COLS; c += 4)
+      *reinterpret_cast<float4*>(&red[g][wave][lane * COLS + c]) =
+          col_ok ? make_float4(acc[g][c], acc[g][c + 1], acc[g][c + 2], acc[g][c + 3])
+                 : make_float4(0.f, 0.f, 0.f, 0.f);
+  lds_barrier();
+  for (int idx = tid; idx < kAGroup * TILE_N / 4; idx += kAThreads) {
+    const int g = idx / (TILE_N / 4), j = (idx - g * (TILE_N / 4)) * 4;
+    if (g < ng) {
+      float4 v = *reinterpret_cast<const float4*>(&red[g][0][j]);
+#pragma unroll
+      for (int w2 = 1; w2 < kAWaves; ++w2) {
+        const float4 t = *reinterpret_cast<const float4*>(&red[g][w2][j]);
+        v.x += t.x; v.y += t.y; v.z += t.z; v.w += t.w;
       }
-      __syncthreads();
-      if (tid < 8 && j0 + tid < p.rank) {
-        float s = 0.f;
-        for (int seg = 0; seg < kAChunk / 8; ++seg) s += useg[seg * 8 + tid];
-        ur[j0 + tid] = s;
-      }
-      __syncthreads();
+      uint32_t r = rows[0];
+#pragma unroll
+      for (int g2 = 1; g2 < kAGroup; ++g2) r = g == g2 ? rows[g2] : r;
+      *reinterpret_cast<float4*>(p.part + (size_t(r) * p.ks + kc) * p.npad + nt * TILE_N + j) = v;
+    }
+  }
+
+  if (ug < ng)
+    for (int j0 = 8; j0 < p.rank; j0 += 8) u_pass(j0, false);
+
+  // 5. TailBufferUpdate: the first tile's block appends the staged x chunk
+  if (nt == 0) {
+    for (int g = 0; g < ng; ++g) {
+      if (p.tail[b0 + g] == nullptr) continue;
+      for (int k = tid; k < kn; k += kAThreads) Elem<IO>::put(p.tail[b0 + g], k0 + k, xs[k][g]);
     }
   }
 }
@@ -201,63 +302,80 @@ template <typename IO, typename ST>
 __global__ void __launch_bounds__(256) adapter_read_reduce_kernel(const AReadParams p) {
   __shared__ float us[8][RWTTT_MAX_RANK];
   __shared__ float u[RWTTT_MAX_RANK];
-  const int b = blockIdx.y;
-  const int n = blockIdx.x * kARedCols + (threadIdx.x & 63);
-  const size_t r = p.row[b];
-  {
-    // u[j] = sum over chunks of the x A shares: eight strided partial sums per
-    // rank column, then those eight in order
-    const int j = threadIdx.x & 31, q = threadIdx.x >> 5;
-    if (j < p.rank) {
-      // chunks q, q + 8, q + 16, ... in order; eight loads in flight at a time
-      float s = 0.f;
-      for (int kc = q; kc < p.ks; kc += 64) {
-        float a[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) a[i] = kc + 8 * i < p.ks ? p.upart[(r * p.ks + kc + 8 * i) * p.rank + j] : 0.f;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) s += a[i];
-      }
-      us[q][j] = s;
-    }
-    __syncthreads();
-    if (int(threadIdx.x) < p.rank) {
-      float s = 0.f;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) s += us[i][threadIdx.x];
-      u[threadIdx.x] = s;
-    }
-    __syncthreads();
-  }
-  // W0 partials: the four waves sum four contiguous quarters of the chunks,
-  // each in chunk order, and the quarters are added in order
   __shared__ float qs[4][kARedCols];
+  const int b = blockIdx.y;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n = blockIdx.x * kARedCols + lane;
+  const int nc = min(n, p.d_model - 1);
+  const size_t r = p.row[b];
   const int per = (p.ks + 3) / 4;
   const int k0 = wave * per, k1 = min(p.ks, k0 + per);
+  const float* q = p.part + r * p.ks * p.npad + nc;
+  const int j = threadIdx.x & 31, qq = threadIdx.x >> 5;
+  const ST* Bm = static_cast<const ST*>(p.state[b]) + size_t(p.d_ff) * p.rank;
+
+  // 1. every first-round request at once, unconditional (indices clamped,
+  //    unused values dropped below): this lane's W0 partials (its wave's
+  //    quarter of the chunks), its x A shares (chunks qq, qq + 8, ...) and the
+  //    first eight B values of its column
+  float a[kARedLoads], t[8], bv[8];
+#pragma unroll
+  for (int i = 0; i < kARedLoads; ++i) a[i] = q[size_t(min(k0 + i, p.ks - 1)) * p.npad];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    t[i] = p.upart[(r * p.ks + min(qq + 8 * i, p.ks - 1)) * p.rank + min(j, p.rank - 1)];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) bv[i] = Elem<ST>::get(Bm, size_t(min(i, p.rank - 1)) * p.d_model + nc);
+
+  // 2. W0 partials: the four waves sum four contiguous quarters of the
+  //    chunks, each in chunk order, and the quarters are added in order
   float s = 0.f;
-  if (n < p.d_model) {
-    const float* q = p.part + r * p.ks * p.npad + n;
-    for (int kc = k0; kc < k1; kc += 8) {
-      float a[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) a[i] = kc + i < k1 ? q[size_t(kc + i) * p.npad] : 0.f;
+  for (int i = 0; i < kARedLoads; ++i) s += k0 + i < k1 ? a[i] : 0.f;
+  for (int kc = k0 + kARedLoads; kc < k1; kc += 8) {
+    float a2[8];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) s += a[i];
-    }
+    for (int i = 0; i < 8; ++i) a2[i] = kc + i < k1 ? q[size_t(kc + i) * p.npad] : 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += a2[i];
   }
   qs[wave][lane] = s;
-  __syncthreads();
-  if (wave != 0 || n >= p.d_model) return;
-  const ST* Bm = static_cast<const ST*>(p.state[b]) + size_t(p.d_ff) * p.rank;
-  float lr = 0.f;
-  for (int j0 = 0; j0 < p.rank; j0 += 8) {
-    float bv[8];
+  // u[j] = sum over chunks of the x A shares: eight strided partial sums per
+  // rank column (chunks qq, qq + 8, qq + 16, ... in order), then those eight in order
+  if (j < p.rank) {
+    float su = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) bv[i] = j0 + i < p.rank ? Elem<ST>::get(Bm, size_t(j0 + i) * p.d_model + n) : 0.f;
+    for (int i = 0; i < 8; ++i) su += qq + 8 * i < p.ks ? t[i] : 0.f;
+    for (int kc = qq + 64; kc < p.ks; kc += 64) {
+      float t2[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) t2[i] = kc + 8 * i < p.ks ? p.upart[(r * p.ks + kc + 8 * i) * p.rank + j] : 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) su += t2[i];
+    }
+    us[qq][j] = su;
+  }
+  lds_barrier();
+  if (int(threadIdx.x) < p.rank) {
+    float su = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) su += us[i][threadIdx.x];
+    u[threadIdx.x] = su;
+  }
+  lds_barrier();
+  if (wave != 0 || n >= p.d_model) return;
+  // 3. + u B, rank columns in order
+  float lr = 0.f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    if (i < p.rank) lr = fmaf(u[i], bv[i], lr);
+  for (int j0 = 8; j0 < p.rank; j0 += 8) {
+    float b2[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) b2[i] = j0 + i < p.rank ? Elem<ST>::get(Bm, size_t(j0 + i) * p.d_model + n) : 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i)
-      if (j0 + i < p.rank) lr = fmaf(u[j0 + i], bv[i], lr);
+      if (j0 + i < p.rank) lr = fmaf(u[j0 + i], b2[i], lr);
   }
   Elem<IO>::put(p.y, r * p.d_model + n, (((qs[0][lane] + qs[1][lane]) + qs[2][lane]) + qs[3][lane]) + lr);
 }
