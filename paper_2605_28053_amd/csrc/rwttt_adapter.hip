@@ -10,6 +10,7 @@
 // are bit-identical whatever group it is batched in.
 
 #include <algorithm>
+#include <type_traits>
 
 #include "rwttt_kernels.h"
 
@@ -386,8 +387,8 @@ __global__ void __launch_bounds__(256) adapter_read_reduce_kernel(const AReadPar
 //
 // 1. adapter_pq_kernel: one block per (evidence row c, slice of 1024 columns
 //    of G / rows of Z) forms that slice's share of P[c][j] = sum_n G[c][n] B[j][n]
-//    or Q[c][j] = sum_k Z[c][k] A[k][j] (four elements per thread, then an
-//    ordered two-level sum over the block).
+//    or Q[c][j] = sum_k Z[c][k] A[k][j] (four elements per thread in order, a
+//    butterfly in each wave, then the four waves in order).
 // 2. adapter_update_kernel: one block per 64 rows k of A or columns n of B;
 //    its four waves take a quarter of the evidence rows each:
 //    A'[k][j] = A[k][j] + eta sum_c Z[c][k] P[c][j] and
@@ -413,8 +414,10 @@ struct AWriteParams {
 
 template <typename IO, typename ST>
 __global__ void __launch_bounds__(256) adapter_pq_kernel(const AWriteParams p) {
-  __shared__ float red[256 * 8];
-  __shared__ float seg[32 * 8];
+  constexpr int EPT = kASlice / 256;       // evidence elements per thread
+  constexpr int kQLoads = 32;              // A requests in flight per thread (Q, power-of-two rank)
+  __shared__ float wsum[4][RWTTT_MAX_RANK];
+  __shared__ float zs[kASlice];
   const int b = blockIdx.z;
   const int c = blockIdx.y;
   const int s = blockIdx.x;                // < sp: a P slice; else a Q slice
@@ -422,52 +425,84 @@ __global__ void __launch_bounds__(256) adapter_pq_kernel(const AWriteParams p) {
   const int i0 = (is_p ? s : s - p.sp) * kASlice;
   const int lim = is_p ? p.d_model : p.d_ff;
   const ST* A = static_cast<const ST*>(p.live[b]);
-  const ST* Bm = A + size_t(p.d_ff) * p.rank;
+  const ST* F = is_p ? A + size_t(p.d_ff) * p.rank : A;   // B for P, A for Q
   const IO* E = static_cast<const IO*>(is_p ? p.g[b] : p.z[b]) + size_t(c) * lim;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   float* out = (is_p ? p.P + ((size_t(p.row[b]) * p.max_chunk + c) * p.sp + s) * p.rank
                      : p.Q + ((size_t(p.row[b]) * p.max_chunk + c) * p.sq + (s - p.sp)) * p.rank);
+  // requests first, unconditional (indices clamped, unused values dropped):
+  // the evidence elements, then each rank pass's factor values
+  float ev[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) ev[e] = Elem<IO>::get(E, min(i0 + e * 256 + tid, lim - 1));
+  const int r = p.rank;
+  if (!is_p && (r & (r - 1)) == 0) {
+    // Q with a power-of-two rank: the slice's A rows are one contiguous run of
+    // 1024 r floats; thread t reads flat elements t, t + 256, ... (consecutive
+    // lanes on consecutive addresses), all of rank column t mod r, against
+    // the Z values of their rows staged in LDS.  Per thread in flat order,
+    // then a butterfly over the lanes of one column, then the waves in order.
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) zs[e * 256 + tid] = i0 + e * 256 + tid < lim ? ev[e] : 0.f;
+    lds_barrier();
+    const int lr = __builtin_ctz(r);
+    const size_t base = size_t(i0) * r, last = size_t(p.d_ff) * r - 1;
+    float acc = 0.f;
+    for (int m0 = 0; m0 < 4 * r; m0 += kQLoads) {
+      float a[kQLoads];
+#pragma unroll
+      for (int q = 0; q < kQLoads; ++q)
+        a[q] = Elem<ST>::get(A, min(base + size_t(tid + 256 * min(m0 + q, 4 * r - 1)), last));
+#pragma unroll
+      for (int q = 0; q < kQLoads; ++q)
+        if (m0 + q < 4 * r) acc = fmaf(zs[(tid + 256 * (m0 + q)) >> lr], a[q], acc);
+    }
+    for (int m = 32; m >= r; m >>= 1) acc += __shfl_xor(acc, m);
+    if (lane < r) wsum[wave][lane] = acc;
+    lds_barrier();
+    if (tid < r) out[tid] = ((wsum[0][tid] + wsum[1][tid]) + wsum[2][tid]) + wsum[3][tid];
+    return;
+  }
   for (int j0 = 0; j0 < p.rank; j0 += 8) {
+    float f[EPT][8];
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      const int ic = min(i0 + e * 256 + tid, lim - 1);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int jj = min(j0 + j, p.rank - 1);
+        f[e][j] = Elem<ST>::get(F, is_p ? size_t(jj) * p.d_model + ic : size_t(ic) * p.rank + jj);
+      }
+    }
     float acc[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[j] = 0.f;
 #pragma unroll
-    for (int e = 0; e < kASlice / 256; ++e) {
-      const int i = i0 + e * 256 + tid;
-      if (i < lim) {
-        const float ev = Elem<IO>::get(E, i);
+    for (int e = 0; e < EPT; ++e) {
+      const float x = i0 + e * 256 + tid < lim ? ev[e] : 0.f;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          if (j0 + j < p.rank) {
-            const float f = is_p ? Elem<ST>::get(Bm, size_t(j0 + j) * p.d_model + i)
-                                 : Elem<ST>::get(A, size_t(i) * p.rank + j0 + j);
-            acc[j] = fmaf(ev, f, acc[j]);
-          }
-        }
-      }
+      for (int j = 0; j < 8; ++j) acc[j] = fmaf(x, f[e][j], acc[j]);
     }
+    // the block's sum: a butterfly in each wave, then the four waves in order
 #pragma unroll
-    for (int j = 0; j < 8; ++j) red[tid * 8 + j] = acc[j];
-    __syncthreads();
-    {
-      const int j = tid & 7, sg = tid >> 3;   // 32 segments of 8 threads
-      float t = 0.f;
+    for (int m = 32; m >= 1; m >>= 1)
 #pragma unroll
-      for (int q = 0; q < 8; ++q) t += red[(sg * 8 + q) * 8 + j];
-      seg[sg * 8 + j] = t;
+      for (int j = 0; j < 8; ++j) acc[j] += __shfl_xor(acc[j], m);
+    if (lane == 0) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) wsum[wave][j] = acc[j];
     }
-    __syncthreads();
-    if (tid < 8 && j0 + tid < p.rank) {
-      float t = 0.f;
-      for (int sg = 0; sg < 32; ++sg) t += seg[sg * 8 + tid];
-      out[j0 + tid] = t;
-    }
-    __syncthreads();
+    lds_barrier();
+    if (tid < 8 && j0 + tid < p.rank)
+      out[j0 + tid] = ((wsum[0][tid] + wsum[1][tid]) + wsum[2][tid]) + wsum[3][tid];
+    lds_barrier();
   }
 }
 
 template <typename IO, typename ST>
 __global__ void __launch_bounds__(256) adapter_update_kernel(const AWriteParams p) {
+  constexpr int RPW = kAPQRows / 4;        // evidence rows per wave and pass
+  constexpr int kPQItems = 2;              // P / Q items per thread whose shares are requested early
   __shared__ float pq[kAPQRows * RWTTT_MAX_RANK];
   __shared__ float part[4][kAUpdCols][RWTTT_MAX_RANK + 1];
   const int b = blockIdx.y;
@@ -476,50 +511,98 @@ __global__ void __launch_bounds__(256) adapter_update_kernel(const AWriteParams 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = (is_a ? int(blockIdx.x) : int(blockIdx.x) - na) * kAUpdCols + lane;
   const int lim = is_a ? p.d_ff : p.d_model;
+  const int ic = min(i, lim - 1);
   const int ns = is_a ? p.sp : p.sq;        // A uses P (slices of N); B uses Q (slices of K)
   const float* src = (is_a ? p.P : p.Q) + size_t(p.row[b]) * p.max_chunk * ns * p.rank;
   const IO* E = static_cast<const IO*>(is_a ? p.z[b] : p.g[b]);
   const int ld = is_a ? p.d_ff : p.d_model;
+  const ST* live = static_cast<const ST*>(p.live[b]);
+  ST* shadow = static_cast<ST*>(p.shadow[b]);
+  auto at_of = [&](int j) {
+    return is_a ? size_t(ic) * p.rank + j : size_t(p.d_ff) * p.rank + size_t(j) * p.d_model + ic;
+  };
+  // the live values of the first two rank columns this thread finishes
+  // (j = wave, wave + 4), requested first
+  float lv[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) lv[h] = Elem<ST>::get(live, at_of(min(wave + 4 * h, p.rank - 1)));
   float acc[RWTTT_MAX_RANK];
 #pragma unroll
   for (int j = 0; j < RWTTT_MAX_RANK; ++j) acc[j] = 0.f;
   for (int c0 = 0; c0 < p.chunk; c0 += kAPQRows) {
     const int cn = min(kAPQRows, p.chunk - c0);
-    __syncthreads();
-    // P / Q rows c0 .. c0+cn: their slice shares added in slice order
-    for (int t = threadIdx.x; t < cn * p.rank; t += 256) {
-      const int cc = t / p.rank, j = t - cc * p.rank;
-      const float* q = src + (size_t(c0 + cc) * ns) * p.rank + j;
-      float v = 0.f;
-      for (int sl = 0; sl < ns; ++sl) v += q[size_t(sl) * p.rank];
-      pq[t] = v;
-    }
-    __syncthreads();
-    // this wave's quarter of the rows, in c order
+    // this wave's quarter of the pass's rows, in c order
     const int q0 = (cn * wave) / 4, q1 = (cn * (wave + 1)) / 4;
-    if (i < lim) {
-      for (int c = q0; c < q1; ++c) {
-        const float ev = Elem<IO>::get(E, size_t(c0 + c) * ld + i);
+    float ev[RPW];
 #pragma unroll
-        for (int j = 0; j < RWTTT_MAX_RANK; ++j)
-          if (j < p.rank) acc[j] = fmaf(ev, pq[c * p.rank + j], acc[j]);
+    for (int r = 0; r < RPW; ++r) ev[r] = Elem<IO>::get(E, size_t(c0 + min(q0 + r, cn - 1)) * ld + ic);
+    // P / Q rows c0 .. c0+cn: their slice shares added in slice order.  The
+    // first kPQItems items of each thread have their first NS shares
+    // requested at once, before the barrier that frees pq (NS: the slice
+    // count rounded up to 4, 8 or 16); further shares are loaded after it.
+    const int items = cn * p.rank;
+    auto stage = [&](auto nsl) {
+      constexpr int NS = decltype(nsl)::value;
+      float sh[kPQItems][NS];
+#pragma unroll
+      for (int it = 0; it < kPQItems; ++it) {
+        const int t = min(int(threadIdx.x) + 256 * it, items - 1);
+        const int cc = t / p.rank, j = t - cc * p.rank;
+        const float* q = src + (size_t(c0 + cc) * ns) * p.rank + j;
+#pragma unroll
+        for (int sl = 0; sl < NS; ++sl) sh[it][sl] = q[size_t(min(sl, ns - 1)) * p.rank];
       }
-    }
+      lds_barrier();   // the previous pass's P / Q rows are no longer read
+      for (int t = threadIdx.x, it = 0; t < items; t += 256, ++it) {
+        const int cc = t / p.rank, j = t - cc * p.rank;
+        const float* q = src + (size_t(c0 + cc) * ns) * p.rank + j;
+        float v = 0.f;
+        if (it < kPQItems) {
+#pragma unroll
+          for (int sl = 0; sl < NS; ++sl) v += sl < ns ? (it == 0 ? sh[0][sl] : sh[kPQItems - 1][sl]) : 0.f;
+        }
+        for (int sl0 = it < kPQItems ? NS : 0; sl0 < ns; sl0 += 8) {
+          float a2[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) a2[k] = q[size_t(min(sl0 + k, ns - 1)) * p.rank];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) v += sl0 + k < ns ? a2[k] : 0.f;
+        }
+        pq[t] = v;
+      }
+    };
+    if (ns <= 4) stage(std::integral_constant<int, 4>{});
+    else if (ns <= 8) stage(std::integral_constant<int, 8>{});
+    else stage(std::integral_constant<int, 16>{});
+    lds_barrier();
+    // this wave's rows in c order; the rank loop is branch-free (columns past
+    // the rank read a valid pq entry and are never stored)
+    auto rows = [&](auto rk) {
+      constexpr int R = decltype(rk)::value;
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) {
+        if (q0 + r < q1) {
+          const float* row = pq + (q0 + r) * p.rank;
+#pragma unroll
+          for (int j = 0; j < R; ++j) acc[j] = fmaf(ev[r], row[min(j, p.rank - 1)], acc[j]);
+        }
+      }
+    };
+    if (p.rank <= 8) rows(std::integral_constant<int, 8>{});
+    else if (p.rank <= 16) rows(std::integral_constant<int, 16>{});
+    else rows(std::integral_constant<int, RWTTT_MAX_RANK>{});
   }
   // the four quarters in wave order
 #pragma unroll
   for (int j = 0; j < RWTTT_MAX_RANK; ++j)
     if (j < p.rank) part[wave][lane][j] = acc[j];
-  __syncthreads();
+  lds_barrier();
   if (i >= lim) return;
-  const ST* live = static_cast<const ST*>(p.live[b]);
-  ST* shadow = static_cast<ST*>(p.shadow[b]);
   const float eta = p.eta;
-  for (int j = wave; j < p.rank; j += 4) {
+  for (int j = wave, h = 0; j < p.rank; j += 4, ++h) {
     const float d = ((part[0][lane][j] + part[1][lane][j]) + part[2][lane][j]) + part[3][lane][j];
-    const size_t at = is_a ? size_t(i) * p.rank + j
-                           : size_t(p.d_ff) * p.rank + size_t(j) * p.d_model + i;
-    Elem<ST>::put(shadow, at, Elem<ST>::get(live, at) + eta * d);
+    const float l = h == 0 ? lv[0] : h == 1 ? lv[1] : Elem<ST>::get(live, at_of(j));
+    Elem<ST>::put(shadow, at_of(j), l + eta * d);
   }
 }
 
