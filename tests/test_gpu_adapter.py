@@ -48,6 +48,8 @@ READ_CASES = [
     (1000, 264, "bf16", "bf16", 1, 4, [2, 1]),
     (520, 1032, "bf16", "f32", 32, 5, [4, 2, 0, 1]),
     (9728, 2560, "bf16", "f32", 8, 8, list(range(8))),
+    # rank above 8 (a second u-share pass) that is not a power of two
+    (3000, 2600, "bf16", "f32", 12, 9, [7, 2, 8, 0, 5, 1, 3, 4, 6]),
 ]
 
 
@@ -92,6 +94,11 @@ WRITE_CASES = [
     (1000, 264, "bf16", "bf16", 8, 64, [1]),
     (520, 1032, "bf16", "f32", 32, 130, [3, 1, 0]),
     (9728, 2560, "bf16", "f32", 8, 64, [1, 3]),
+    # ranks that are not powers of two (Q through the per-row path) in the
+    # 8- and 16-wide rank classes of the update, and a chunk of two passes
+    (2104, 1096, "bf16", "f32", 5, 33, [2, 0]),
+    (2104, 1096, "bf16", "bf16", 12, 70, [3]),
+    (1000, 264, "f32", "f32", 16, 20, [1, 2]),
 ]
 
 
