@@ -247,17 +247,29 @@ def test_bench_refuses_more_than_one_gpu():
     assert "one GPU" in r.stderr
 
 
-def test_bench_traffic_applies_only_to_its_shape_and_source():
+def test_bench_traffic_applies_only_to_its_shape_and_source(tmp_path, monkeypatch):
     """The PMC traffic table is reported only for the READ shape, group sizes and
-    kernel source it was measured on."""
+    kernel source it was measured on (a table written here, keyed like the
+    committed one)."""
+    import json
     import bench
     from rwttt_inputs import workload
-    rec = lambda b, n: ("read", b, 0, None, None, n)
     mixed, prefill, ragged = workload(2), workload(4), workload(3)
-    t = bench.measured_traffic([rec(8, 3), rec(7, 1)], mixed)
-    assert t is not None and 7e8 < t < 9e8
-    assert bench.measured_traffic([rec(8, 1)], prefill) is None
-    assert bench.measured_traffic([rec(16, 1)], ragged) is None
+    table = {"kernel_source_sha256": bench.kernel_source_sha(), "workload": mixed.name,
+             "read_shape": {"d_model": mixed.d_model, "d_ff": mixed.d_ff,
+                            "io": mixed.io_dtype, "state": mixed.state_dtype},
+             "read_call_bytes_by_group_size": {"8": {"fetch": 800.0, "write": 3.0},
+                                               "7": {"fetch": 700.0, "write": 2.0}}}
+    (tmp_path / "profiles").mkdir()
+    (tmp_path / "profiles" / "hbm_traffic__mixed8-4b-36L.json").write_text(json.dumps(table))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_sha", lambda: table["kernel_source_sha256"])
+    rec = lambda b, n: ("read", b, 0, None, None, n)
+    assert bench.measured_traffic([rec(8, 3), rec(7, 1)], mixed) == (3 * 803.0 + 702.0) / 4
+    assert bench.measured_traffic([rec(8, 1)], prefill) is None      # another shape
+    assert bench.measured_traffic([rec(16, 1)], ragged) is None      # a group size not measured
+    monkeypatch.setattr(bench, "kernel_source_sha", lambda: "0" * 64)
+    assert bench.measured_traffic([rec(8, 1)], mixed) is None        # other kernel code
     # comments and indentation do not change the key, code does
     code = "int a; // x\n  int b;\n\n"
     assert bench.code_lines(code) == ["int a;", "int b;"]
