@@ -296,39 +296,53 @@ def run_gpu(args, wl, layers):
 
 
 def run_cpu_baseline(args, wl, kept):
-    """The oracle as it stands, on steps [0, S) of the same trace, a layer subset."""
+    """The oracle as it stands, on steps [0, S) of the same trace, a layer subset,
+    with every BLAS thread the host gives it; then a shorter sample on one thread."""
     import oracle as O
     from rwttt_inputs import TensorSource, build_trace
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()
                             if i.get("user_api") == "blas"] or [1])
     except Exception:
+        threadpool_limits = None
         blas_threads = os.cpu_count()
     layers = [l for l in args.cpu_layers if l < wl.n_layers] or [0]
     steps = range(min(args.cpu_steps, wl.n_steps))
     trace = build_trace(wl, len(steps))
     src = TensorSource(wl)
-    table = None
-    if not args.rank:
-        table = O.OwnerTable(wl.n_owners, layers)
-        for r in range(wl.n_owners):
-            for l in layers:
-                arr = kept.get((r, l))
-                table.D[(r, l)] = O.widen(arr if arr is not None else src.dw_init(r, l),
-                                          wl.state_dtype)
-    for t in steps:                       # draw the inputs outside the timed window
-        src.x_step(t)
-    t0 = time.perf_counter()
-    records, _ = O.run_trace(wl, trace, src, steps=steps, layers=layers, table=table,
-                             rank=args.rank)
-    dt = time.perf_counter() - t0
-    tokens = sum(len(rec.y) for rec in records) / len(layers)
-    scale = wl.n_layers / len(layers)
-    return dict(value=tokens / (dt * scale), unit="tok/s", cores=int(blas_threads), kind="oracle",
-                sample=(f"float64 numpy oracle on decode steps 0-{len(steps) - 1} of the same "
-                        f"trace, layers {layers} of {wl.n_layers}, all {wl.n_owners} owners; "
-                        f"{dt:.2f} s measured, scaled x{scale:g} to all layers"))
+
+    def timed(steps, layers):
+        table = None
+        if not args.rank:
+            table = O.OwnerTable(wl.n_owners, layers)
+            for r in range(wl.n_owners):
+                for l in layers:
+                    arr = kept.get((r, l))
+                    table.D[(r, l)] = O.widen(arr if arr is not None else src.dw_init(r, l),
+                                              wl.state_dtype)
+        for t in steps:                   # draw the inputs outside the timed window
+            src.x_step(t)
+        t0 = time.perf_counter()
+        records, _ = O.run_trace(wl, trace, src, steps=steps, layers=layers, table=table,
+                                 rank=args.rank)
+        dt = time.perf_counter() - t0
+        tokens = sum(len(rec.y) for rec in records) / len(layers)
+        return tokens / (dt * wl.n_layers / len(layers)), dt
+
+    value, dt = timed(steps, layers)
+    out = dict(value=value, unit="tok/s", cores=int(blas_threads), kind="oracle",
+               sample=(f"float64 numpy oracle on decode steps 0-{len(steps) - 1} of the same "
+                       f"trace, layers {layers} of {wl.n_layers}, all {wl.n_owners} owners; "
+                       f"{dt:.2f} s measured, scaled x{wl.n_layers / len(layers):g} to all layers"))
+    if threadpool_limits is not None:
+        steps1 = range(min(len(steps), 10))
+        with threadpool_limits(limits=1):
+            v1, dt1 = timed(steps1, layers[:1])
+        out["single_thread"] = dict(value=v1, unit="tok/s", cores=1,
+                                    sample=f"decode steps 0-{len(steps1) - 1}, layer {layers[0]}; "
+                                           f"{dt1:.2f} s measured")
+    return out
 
 
 def time_library_write(torch, wl, wr, calls=20):
