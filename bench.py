@@ -393,6 +393,60 @@ def time_library_write(torch, wl, wr, calls=20):
             "this_write_avg_us": round(wr["avg_us"], 2)}
 
 
+def pmc_summary(dirs):
+    """Per-dispatch HBM bytes of the READ and fused-WRITE calls from rocprofv3 PMC
+    databases, as the table measured_traffic() reads.  `dirs` holds the
+    directories of four runs: the plain 1 GiB copy and the bench, each once with
+    FETCH_SIZE and once with WRITE_SIZE (see profiles/hbm_traffic__mixed8-4b-36L.md).
+    Each counter is scaled by what it reads for the copy of known size."""
+    import glob
+    import re
+    import sqlite3
+    from collections import defaultdict
+    from rwttt_inputs import workload
+
+    def rows(d):
+        (db,) = glob.glob(os.path.join(d, "*_results.db"))
+        q = ("select p.name, p.counter_value, k.grid_x, k.grid_y from pmc_events p "
+             "join kernels k on k.dispatch_id = p.dispatch_id")
+        return sqlite3.connect(db).execute(q).fetchall()
+
+    scale, per = {}, {}
+    for cn in ("FETCH_SIZE", "WRITE_SIZE"):
+        copy = [v for n, v, _, _ in rows(dirs[f"copy_{cn}"]) if "copy" in n.lower()]
+        scale[cn] = (1 << 30) / (max(copy) * 1024.0)
+        agg = defaultdict(list)
+        for n, v, gx, gy in rows(dirs[f"bench_{cn}"]):
+            m = re.search(r"(\w+_kernel)\b", n)
+            agg[(m.group(1) if m else n, gx, gy)].append(v * 1024.0 * scale[cn])
+        per[cn] = agg
+    wl = workload(2)
+    pairs = ((wl.d_ff + 255) // 256) * ((wl.d_model + 255) // 256)
+    pairs8 = (pairs + 7) // 8 * 8
+    # a READ call of B owners = one read_partial_kernel launch (grid of B slots)
+    # + one read_reduce_kernel launch (grid_y = B); a reduce of grid_y 1 with no
+    # READ partner is the fused WRITE token's
+    table = {}
+    for cn in per:
+        for (name, gx, gy), vs in per[cn].items():
+            if name == "read_partial_kernel":
+                e = table.setdefault(str(gx // 256 // pairs8), {"fetch": 0.0, "write": 0.0})
+                e["fetch" if cn == "FETCH_SIZE" else "write"] += sum(vs) / len(vs)
+    for cn in per:
+        for (name, gx, gy), vs in per[cn].items():
+            if name == "read_reduce_kernel" and str(gy) in table:
+                table[str(gy)]["fetch" if cn == "FETCH_SIZE" else "write"] += sum(vs) / len(vs)
+    wr = {cn: [sum(vs) / len(vs) for (name, _, _), vs in per[cn].items()
+               if name == "write_stream_kernel"] for cn in per}
+    return {"kernel_source_sha256": kernel_source_sha(), "workload": wl.name,
+            "read_shape": {"d_model": wl.d_model, "d_ff": wl.d_ff, "io": wl.io_dtype,
+                           "state": wl.state_dtype},
+            "calibration": {"copy_bytes": 1 << 30, "fetch_scale": scale["FETCH_SIZE"],
+                            "write_scale": scale["WRITE_SIZE"]},
+            "read_call_bytes_by_group_size": table,
+            "write_call_bytes": {"fetch": max(wr["FETCH_SIZE"]), "write": max(wr["WRITE_SIZE"])}}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -414,9 +468,18 @@ def main():
     ap.add_argument("--library-write", choices=["on", "off"], default="off",
                     help="also time torch.baddbmm (the vendor GEMM library) on the same "
                          "update as one WRITE call, for a bf16 state (context, not the value)")
+    ap.add_argument("--pmc-summary", metavar="DIR",
+                    help="only summarise the PMC runs under DIR (pmc_copy_FETCH_SIZE, "
+                         "pmc_bench_FETCH_SIZE, ... subdirectories) into the traffic table JSON")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
                     help="only run 5 plain device copies of BYTES each (HBM counter calibration)")
     args = ap.parse_args()
+
+    if args.pmc_summary:
+        dirs = {f"{k}_{cn}": os.path.join(args.pmc_summary, f"pmc_{k}_{cn}")
+                for k in ("copy", "bench") for cn in ("FETCH_SIZE", "WRITE_SIZE")}
+        print(json.dumps(pmc_summary(dirs), indent=1))
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:

@@ -276,6 +276,47 @@ def test_bench_traffic_applies_only_to_its_shape_and_source(tmp_path, monkeypatc
     assert bench.code_lines("int a; // y\nint b;") == bench.code_lines(code)
 
 
+def test_bench_pmc_summary_scales_and_groups_by_call(tmp_path):
+    """The PMC summariser scales each counter by the copy calibration and sums a
+    READ call's partial and reduce launches per group size (synthetic databases
+    with the rocpd columns it reads)."""
+    import sqlite3
+    import bench
+    ns = "void rwttt::(anonymous namespace)::"
+    part = ns + "read_partial_kernel<unsigned short, float>(rwttt::(anonymous namespace)::ReadParams)"
+    red = ns + "read_reduce_kernel<unsigned short>(rwttt::(anonymous namespace)::ReadParams)"
+    wst = ns + "write_stream_kernel<float, true>(rwttt::(anonymous namespace)::WriteParams)"
+    copy = "__amd_rocclr_copyBuffer"
+
+    def db(path, rows):
+        path.mkdir()
+        c = sqlite3.connect(str(path / "x_results.db"))
+        c.execute("create table pmc_events (dispatch_id int, name text, counter_value real)")
+        c.execute("create table kernels (dispatch_id int, grid_x int, grid_y int)")
+        for i, (name, v, gx, gy) in enumerate(rows):
+            c.execute("insert into pmc_events values (?, ?, ?)", (i, name, v))
+            c.execute("insert into kernels values (?, ?, ?)", (i, gx, gy))
+        c.commit()
+
+    kib = (1 << 30) / 1024
+    db(tmp_path / "pmc_copy_FETCH_SIZE", [(copy, kib / 2, 1, 1)])    # reads half: scale 2
+    db(tmp_path / "pmc_copy_WRITE_SIZE", [(copy, kib, 1, 1)])
+    blocks8 = 384 * 8 * 256
+    db(tmp_path / "pmc_bench_FETCH_SIZE", [(part, 100.0, blocks8, 1), (part, 300.0, blocks8, 1),
+                                           (red, 10.0, 10240, 8), (red, 1.0, 10240, 1),
+                                           (wst, 50.0, 122880, 1)])
+    db(tmp_path / "pmc_bench_WRITE_SIZE", [(part, 4.0, blocks8, 1), (red, 2.0, 10240, 8),
+                                           (red, 7.0, 10240, 1), (wst, 60.0, 122880, 1)])
+    dirs = {f"{k}_{cn}": str(tmp_path / f"pmc_{k}_{cn}")
+            for k in ("copy", "bench") for cn in ("FETCH_SIZE", "WRITE_SIZE")}
+    out = bench.pmc_summary(dirs)
+    assert out["calibration"]["fetch_scale"] == 2.0 and out["calibration"]["write_scale"] == 1.0
+    assert out["read_call_bytes_by_group_size"] == {"8": {"fetch": (200.0 + 10.0) * 2 * 1024,
+                                                          "write": (4.0 + 2.0) * 1024}}
+    assert out["write_call_bytes"] == {"fetch": 50.0 * 2 * 1024, "write": 60.0 * 1024}
+    assert out["kernel_source_sha256"] == bench.kernel_source_sha()
+
+
 def test_plain_c_client_builds_against_the_header_and_runs(tmp_path):
     """The header is C (not only C++): a C11 client compiles with gcc, links the
     library and drives planning and the owner table on a host-only context."""
