@@ -295,6 +295,23 @@ def run_gpu(args, wl, layers):
                 writes=writes, kept=kept, steps=len(timed), warmup=len(warm))
 
 
+def host_info():
+    """The host the oracle ran on: logical CPUs, CPU model and memory."""
+    info = {"nproc": os.cpu_count()}
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                info["cpu"] = line.split(":", 1)[1].strip()
+                break
+        for line in open("/proc/meminfo"):
+            if line.startswith("MemTotal"):
+                info["ram_gb"] = round(int(line.split()[1]) / 1024 ** 2, 1)
+                break
+    except OSError:
+        pass
+    return info
+
+
 def run_cpu_baseline(args, wl, kept):
     """The oracle as it stands, on steps [0, S) of the same trace, a layer subset,
     with every BLAS thread the host gives it; then a shorter sample on one thread."""
@@ -335,6 +352,7 @@ def run_cpu_baseline(args, wl, kept):
                sample=(f"float64 numpy oracle on decode steps 0-{len(steps) - 1} of the same "
                        f"trace, layers {layers} of {wl.n_layers}, all {wl.n_owners} owners; "
                        f"{dt:.2f} s measured, scaled x{wl.n_layers / len(layers):g} to all layers"))
+    out["host"] = host_info()
     if threadpool_limits is not None:
         steps1 = range(min(len(steps), 10))
         with threadpool_limits(limits=1):
