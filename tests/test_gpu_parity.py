@@ -65,6 +65,7 @@ READ_CASES = [
     (520, 1032, "bf16", "f32", 20, list(range(19, -1, -1))[:17]),
     (264, 520, "f32", "bf16", 3, [2]),
     (9728, 2560, "bf16", "f32", 8, list(range(8))),
+    (264, 136, "bf16", "f32", 64, list(range(63, -1, -1))),   # the largest group
 ]
 
 
@@ -121,12 +122,14 @@ WRITE_CASES = [
     (520, 264, "bf16", "f32", 150, [1]),
     (128, 64, "bf16", "f32", 32, [0, 1, 2, 3]),
     (9728, 2560, "bf16", "f32", 64, [1]),
+    (264, 136, "bf16", "f32", 33, [11, 4, 0, 7, 2, 9, 5, 1, 10, 3, 8, 6]),   # 12 owners, stream path
+    (264, 136, "bf16", "bf16", 130, [9, 2, 5, 0, 7, 3, 8, 1, 6, 4]),        # 10 owners, GEMM path
 ]
 
 
 @pytest.mark.parametrize("d_ff,d_model,io,state,chunk,group", WRITE_CASES)
 def test_write_commit_rollback_match_oracle(d_ff, d_model, io, state, chunk, group):
-    n_owners = 4
+    n_owners = max(4, max(group) + 1)
     wl = small_workload(d_ff, d_model, io, state, n_owners, eta=0.05)
     say("write", d_ff, d_model, io, state, chunk, group)
     src = TensorSource(wl)
