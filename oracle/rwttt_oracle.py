@@ -43,6 +43,8 @@ from dataclasses import dataclass, field
 import numpy as np
 
 READ, WRITE = 0, 1
+# backend state types tau (Section 4.1 payloads; Section 4.4 backend instantiations)
+FAST_WEIGHT, DELTA_ADAPTER = 0, 1
 
 OK = 0
 DEFERRED = 1
@@ -341,7 +343,9 @@ def run_trace(wl, trace, src, steps=None, layers=None, cols=None,
     for t in steps:
         items = trace[t]
         by_owner = {it.owner: it for it in items}
-        events = [Event(it.owner, 0, sigma(wl, it.effect, it.chunk), 0, it.effect,
+        # tau is the owners' state type: every owner of a run holds the same kind
+        tau = DELTA_ADAPTER if rank else FAST_WEIGHT
+        events = [Event(it.owner, tau, sigma(wl, it.effect, it.chunk), 0, it.effect,
                         table.V[it.owner], t) for it in items]
         p = plan(events, table.V, table.dirty, wl.n_owners, t, B, w)
         ys = {}

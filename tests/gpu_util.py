@@ -58,11 +58,12 @@ def host_f64(t, dtype):
     return O.widen(to_host(t, dtype), dtype)
 
 
-def run_gpu_trace(wl, trace, src, steps, layers=None, cols=None, fail_hook=None, stream=None):
+def run_gpu_trace(wl, trace, src, steps, layers=None, cols=None, fail_hook=None, stream=None,
+                  backend=0, rank=0):
     """Run steps of a trace through Session.step (the serving loop) and collect
     (StepResult, versions after the step, {(owner, layer): y row}) per step."""
     layers = list(range(wl.n_layers)) if layers is None else list(layers)
-    sess = Session(wl, src, layers)
+    sess = Session(wl, src, layers, backend=backend, rank=rank)
     out = []
     tdt = torch.float32 if wl.io_dtype == "f32" else torch.bfloat16
     for t in steps:

@@ -14,9 +14,9 @@ import pytest
 import torch
 
 import oracle as O
-from rwttt_inputs import READ, WRITE, TensorSource, draw
-from tests.gpu_util import (R, Session, all_slot_hashes, host_f64, read_group, say, slot_hash,
-                            small_workload, to_device, write_group)
+from rwttt_inputs import READ, WRITE, TensorSource, build_trace, draw, workload
+from tests.gpu_util import (R, Session, all_slot_hashes, host_f64, plan_tuples, read_group,
+                            run_gpu_trace, say, slot_hash, small_workload, to_device, write_group)
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
@@ -160,6 +160,29 @@ def test_adapter_write_token_commit_rollback_match_oracle(d_ff, d_model, io, sta
         torch.cuda.synchronize()
         assert slot_hash(solo.shadow(r, 0)) == sh[r]
         solo.close()
+
+
+@pytest.mark.parametrize("rank", [3, 4])
+def test_adapter_tiny_trace_matches_oracle(rank):
+    """The tiny fp32 trace (a WRITE every 4 steps, the 3rd write of owner 1
+    forced to fail) through the serving loop with rank-r adapter state: plans,
+    versions and every token against the oracle's sequential run, and the final
+    factors."""
+    wl = workload(0)
+    trace, src = build_trace(wl), TensorSource(wl)
+    say("adapter tiny trace", wl.name, rank)
+    ref, table = O.run_trace(wl, trace, src, rank=rank)
+    sess, got = run_gpu_trace(wl, trace, src, range(wl.n_steps), backend=ADA, rank=rank)
+    for rec, (res, versions, ys) in zip(ref, got):
+        assert plan_tuples(res) == [(g.key, g.owners) for g in rec.plan.groups]
+        assert versions == rec.versions
+        for k, v in rec.y.items():
+            assert O.max_rel_floor(ys[k], v) <= out_tol(wl.io_dtype), (rec.step, k)
+    for r in range(wl.n_owners):
+        gA, gB = factors_f64(sess, sess.live(r, 0), wl.state_dtype)
+        A, B = table.D[(r, 0)]
+        assert O.rel_frobenius(gA, A) <= STATE_TOL and O.rel_frobenius(gB, B) <= STATE_TOL
+    assert sess.versions() == [4, 3]
 
 
 def test_adapter_sixteen_writes_full_shape():

@@ -607,15 +607,19 @@ def test_adapter_write_first_order_moves_the_product_like_the_fast_weight_rule()
 
 def test_adapter_trace_equals_per_request_sequential_application():
     """The adapter run plans and versions exactly like the fast-weight run (the
-    plan never looks at the payload), and its outputs equal each request walked
-    alone through adapter_read / adapter_write in order."""
+    plan never looks at the payload; only the backend type in the key differs),
+    and its outputs equal each request walked alone through adapter_read /
+    adapter_write in order."""
     wl, rank = workload(0), 3
     trace, src = build_trace(wl), TensorSource(wl)
     fw, _ = O.run_trace(wl, trace, src)
     ad, table = O.run_trace(wl, trace, src, rank=rank)
     assert [r.versions for r in ad] == [r.versions for r in fw]
-    assert [[(g.key, g.owners) for g in r.plan.groups] for r in ad] == \
-           [[(g.key, g.owners) for g in r.plan.groups] for r in fw]
+    assert all(g.key[1] == O.DELTA_ADAPTER for r in ad for g in r.plan.groups)
+    assert all(g.key[1] == O.FAST_WEIGHT for r in fw for g in r.plan.groups)
+    drop_tau = lambda k: (k[0],) + tuple(k[2:])
+    assert [[(drop_tau(g.key), g.owners) for g in r.plan.groups] for r in ad] == \
+           [[(drop_tau(g.key), g.owners) for g in r.plan.groups] for r in fw]
     W0 = O.widen(src.w0(0), "f32")
     for r in range(wl.n_owners):
         a, b = src.adapter_init(r, 0, rank)
