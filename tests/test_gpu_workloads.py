@@ -18,7 +18,7 @@ import torch
 
 import oracle as O
 from rwttt_inputs import TensorSource, build_trace, workload
-from tests.gpu_util import host_f64, plan_tuples, run_gpu_trace, say
+from tests.gpu_util import R, host_f64, plan_tuples, run_gpu_trace, say
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
@@ -88,17 +88,21 @@ def test_prefill8b_bf16_state_sampled():
     assert table.V == [8] * 8
 
 
-def test_two_stream_serving_is_bit_identical_to_one_stream():
-    """READ and WRITE groups on two joined streams give the same bits as one stream."""
+@pytest.mark.parametrize("rank", [0, 8])
+def test_two_stream_serving_is_bit_identical_to_one_stream(rank):
+    """READ and WRITE groups on two joined streams give the same bits as one
+    stream, with fast-weight state (rank 0) and with rank-8 adapter state."""
     from paper_2605_28053_amd.serving import StreamPair
     wl = workload(3)
     src = TensorSource(wl, memo=True)
-    src.prefetch(range(wl.n_owners), [0], 16)
+    if not rank:
+        src.prefetch(range(wl.n_owners), [0], 16)
     trace = build_trace(wl, 12)
-    one, out1 = run_gpu_trace(wl, trace, src, range(12))
+    backend = R.RWTTT_DELTA_ADAPTER if rank else R.RWTTT_FAST_WEIGHT
+    one, out1 = run_gpu_trace(wl, trace, src, range(12), backend=backend, rank=rank)
     pair = StreamPair()
     pair.wait_for_current()
-    two, out2 = run_gpu_trace(wl, trace, src, range(12), stream=pair)
+    two, out2 = run_gpu_trace(wl, trace, src, range(12), stream=pair, backend=backend, rank=rank)
     for (r1, v1, y1), (r2, v2, y2) in zip(out1, out2):
         assert plan_tuples(r1) == plan_tuples(r2) and v1 == v2
         assert set(y1) == set(y2)
