@@ -235,3 +235,22 @@ def test_adapter_tail_and_fork():
     torch.cuda.synchronize()
     assert slot_hash(sess.live(1, 0)) == slot_hash(sess.live(2, 0))
     assert sess.versions() == [0, 1, 1]
+    # checkpoint owner 2's committed factors to pinned host memory, move the owner
+    # on by another committed write, then resume: factors and version come back exactly
+    nbytes = sess.live(2, 0).numel() * sess.live(2, 0).element_size()
+    host = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    st, v = R.rwttt_checkpoint(sess.ctx, 2, [host.data_ptr()], torch.cuda.current_stream().cuda_stream)
+    assert st == R.RWTTT_OK and v == 1
+    torch.cuda.synchronize()
+    saved = slot_hash(sess.live(2, 0))
+    Z2 = to_device(draw((chunk, d_ff), 1.0, "bf16", wl.seed, (93,), absval=True), "bf16")
+    assert write_group(sess, [2], 0, chunk, [Z2], [gd]) == R.RWTTT_OK
+    assert R.rwttt_commit(sess.ctx, [2]) == R.RWTTT_OK
+    torch.cuda.synchronize()
+    assert sess.versions() == [0, 1, 2] and slot_hash(sess.live(2, 0)) != saved
+    assert R.rwttt_resume(sess.ctx, 2, [host.data_ptr()], v,
+                          torch.cuda.current_stream().cuda_stream) == R.RWTTT_OK
+    torch.cuda.synchronize()
+    assert sess.versions() == [0, 1, 1] and slot_hash(sess.live(2, 0)) == saved
+    # the forked child kept its own copy throughout
+    assert slot_hash(sess.live(1, 0)) == saved
