@@ -589,7 +589,7 @@ write_gemm_kernel(const WriteParams p) {
   uint16_t* reg[2] = {s0, s0};
   auto live_copy = [&](uint16_t* dst, int hf) {
     const int row0 = m0 + wave * 64 + hf * 32;
-    const int rows = max(0, min(32, p.d_ff - row0));
+    const int rows = __builtin_amdgcn_readfirstlane(max(0, min(32, p.d_ff - row0)));   // wave-uniform
     const i32x4_t lr = gemm_rsrc(live + size_t(min(row0, p.d_ff)) * p.d_model, rows * p.d_model * 2);
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
@@ -691,7 +691,7 @@ write_gemm_kernel(const WriteParams p) {
       asm volatile("" ::: "memory");
       if (hf == 0) gemm_wait_vm<0>();
       const int row0 = m0 + wave * 64 + hf * 32;
-      const int rows = max(0, min(32, p.d_ff - row0));
+      const int rows = __builtin_amdgcn_readfirstlane(max(0, min(32, p.d_ff - row0)));   // wave-uniform
       const __amdgpu_buffer_rsrc_t sr = __builtin_amdgcn_make_buffer_rsrc(
           shadow + size_t(min(row0, p.d_ff)) * p.d_model, (short)0, rows * p.d_model * 2, 0x00020000);
 #pragma unroll
