@@ -280,12 +280,15 @@ write_stream_kernel(const WriteParams p) {
   const uint16_t* W0 = static_cast<const uint16_t*>(p.w0);
   const uint16_t* X = static_cast<const uint16_t*>(p.x) + size_t(p.row[b]) * p.d_ff;
 
-  // G tile [C ranks][256 n] -> gt[n][rank], 32 columns per thread pass
-  for (int j = 0; j < kSTN / 32; ++j) {
-    uint4 ga, gb;
-    stream_load_pair(G, p.d_model, p.d_model, p.chunk, n0 + j * 32, tid, ga, gb);
-    stream_store_pair(gt, tid, j * 32, ga, gb);
-  }
+  // G tile [C ranks][256 n] -> gt[n][rank], 32 columns per thread pass.
+  // Every G request and every request of the first item goes out before
+  // any of them is used, so the block's start costs one memory round trip
+  // (each use of a value loaded under a lane condition waits for all
+  // outstanding loads).
+  uint4 ga[kSTN / 32], gb[kSTN / 32];
+#pragma unroll
+  for (int j = 0; j < kSTN / 32; ++j)
+    stream_load_pair(G, p.d_model, p.d_model, p.chunk, n0 + j * 32, tid, ga[j], gb[j]);
 
   // the first item's operands
   float yacc[4] = {0.f, 0.f, 0.f, 0.f};
@@ -299,6 +302,8 @@ write_stream_kernel(const WriteParams p) {
     if (part * kSTM + wave * RPW < p.d_ff)
       xq = *reinterpret_cast<const uint4*>(X + part * kSTM + wave * RPW);
   }
+#pragma unroll
+  for (int j = 0; j < kSTN / 32; ++j) stream_store_pair(gt, tid, j * 32, ga[j], gb[j]);
 
   for (int mt = part; mt < p.mt; mt += p.parts) {
     const int m0 = mt * kSTM;
