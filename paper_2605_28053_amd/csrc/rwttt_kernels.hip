@@ -206,7 +206,20 @@ constexpr int kSTM = 32;                 // rows per item
 constexpr int kSTN = 256;                // columns per tile
 constexpr int kSMaxC = 64;               // largest chunk on this path
 constexpr int kSPitch = kSMaxC + 8;      // bf16 per staged rank row (144 B: 16 rows hit 16 bank groups)
-constexpr int kSParts = 48;              // row-tile partitions per (owner, column tile)
+constexpr int kSParts = 64;              // most row-tile partitions per (owner, column tile)
+constexpr int kSSlots = 512;             // blocks of this kernel resident at once (256 CUs x 2)
+
+// Row-tile partitions per (owner, column tile), from the shape alone, so that
+// an owner's token partials are added in the same order in any group: as many
+// as let one owner's blocks fill one round of the block slots, then the fewest
+// that keep the largest partition at the same number of items.
+int stream_parts(int d_ff, int d_model) {
+  const int mt = (d_ff + kSTM - 1) / kSTM;
+  const int ntl = (d_model + kSTN - 1) / kSTN;
+  const int pmax = std::max(1, std::min(std::min(kSParts, mt), kSSlots / ntl));
+  const int items = (mt + pmax - 1) / pmax;
+  return (mt + items - 1) / items;
+}
 
 template <typename T>
 __device__ __forceinline__ void stream_load_rows(const T* base, int d_ff, int d_model, int m0,
@@ -896,7 +909,7 @@ hipError_t launch_write_t(const WriteLaunch& L, hipStream_t stream) {
     p.mt = (L.d_ff + kSTM - 1) / kSTM;
     p.ntl = (L.d_model + kSTN - 1) / kSTN;
     // partitions of an owner's row tiles: fixed by the shape, never by the group
-    p.parts = std::min(geo.tparts, p.mt);
+    p.parts = std::min(stream_parts(L.d_ff, L.d_model), geo.tparts);
     p.npadw = geo.tnpad;
     p.tpart = token ? reinterpret_cast<float*>(static_cast<char*>(L.workspace) + geo.token_offset) : nullptr;
     const unsigned pairs8 = unsigned((p.ntl * p.parts + 7) / 8 * 8);
