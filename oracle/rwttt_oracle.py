@@ -387,6 +387,8 @@ def run_trace(wl, trace, src, steps=None, layers=None, cols=None,
 # --------------------------------------------------------------------------
 
 def rel_frobenius(a, ref):
+    """||a - ref||_F / ||ref||_F over all elements, in float64; the absolute
+    error norm when the reference is all zero."""
     a = np.asarray(a, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     den = np.linalg.norm(ref)
@@ -395,7 +397,12 @@ def rel_frobenius(a, ref):
 
 
 def max_rel_floor(a, ref, floor_frac=1e-2):
-    """max_i |a_i - b_i| / max(|b_i|, floor_frac * rms(b))."""
+    """max_i |a_i - b_i| / max(|b_i|, floor_frac * rms(b)) over all elements.
+
+    The floor keeps an element that nearly cancels from dominating a relative
+    measure; an all-zero reference (rms 0) gives the absolute error, and an
+    empty one 0.
+    """
     a = np.asarray(a, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     if ref.size == 0:

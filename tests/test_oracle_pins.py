@@ -299,6 +299,40 @@ def test_plan_wait_bound_holds_over_time():
             assert waits and max(waits) <= w
 
 
+def test_plan_bounded_groups_with_mixed_ready_steps_by_hand():
+    """B = 2, w = 3, events of one READ key that became ready at different steps,
+    plus two WRITE keys.  Members are taken in (ready step, owner) order, so the
+    oldest events fill the full groups first (eq. wait-budget: the oldest is the
+    one closest to its bound) and ties in ready step go by owner id; the
+    remainder waits until its oldest member has waited w steps."""
+    events = [_ev(1, ready=5), _ev(0, ready=3), _ev(4, ready=1), _ev(2, ready=3), _ev(3, ready=2),
+              _ev(6, WRITE, 16, ready=4), _ev(5, WRITE, 16, ready=4), _ev(7, WRITE, 64, ready=0),
+              _ev(8, WRITE, 16, ready=5)]
+    V, dirty = [0] * 9, [False] * 9
+    p = O.plan(events, V, dirty, 9, 5, 2, 3)
+    assert [(g.effect, g.key[2], g.owners) for g in p.groups] == [
+        (READ, 0, [4, 3]), (READ, 0, [0, 2]),     # ready 1, 2 | ready 3, 3 (owner order)
+        (WRITE, 16, [5, 6]),                      # ready 4, 4: owner order
+        (WRITE, 64, [7]),                         # alone, but waited 5 >= 3 steps
+    ]
+    # owner 1 (READ, ready 5) and owner 8 (WRITE C=16, ready 5) have waited 0 steps
+    assert sorted(events[i].owner for i in p.deferred) == [1, 8]
+    assert [p.ev_status[i] for i in range(9)] == [O.DEFERRED, O.OK, O.OK, O.OK, O.OK,
+                                                  O.OK, O.OK, O.OK, O.DEFERRED]
+    # three steps later the two remainders have waited w steps and are issued
+    q = O.plan([events[0], events[8]], V, dirty, 9, 8, 2, 3)
+    assert [(g.effect, g.key[2], g.owners) for g in q.groups] == [(READ, 0, [1]), (WRITE, 16, [8])]
+    assert q.deferred == []
+    # one step earlier they are still deferred
+    q = O.plan([events[0], events[8]], V, dirty, 9, 7, 2, 3)
+    assert q.groups == [] and sorted(q.deferred) == [0, 1]
+    # B = 3: the remainder [2] keeps its own oldest ready step (3): at step 5 it
+    # has waited 2 < 3 steps and is deferred, although owner 4 (ready 1) waited 4
+    p = O.plan(events[:5], V, dirty, 9, 5, 3, 3)
+    assert [g.owners for g in p.groups] == [[4, 3, 0]]
+    assert sorted(events[i].owner for i in p.deferred) == [1, 2]
+
+
 def test_uniform_trace_counts_match_paper():
     g = json.load(open(os.path.join(GOLDEN, "uniform_trace.json")))
     S, T, C = g["streams"], g["decode_tokens"], g["ttt_chunk"]
@@ -636,3 +670,48 @@ def test_adapter_trace_equals_per_request_sequential_application():
                 A, B = A.astype(np.float32).astype(np.float64), B.astype(np.float32).astype(np.float64)
         assert O.rel_frobenius(table.D[(r, 0)][0], A) < 1e-6
         assert O.rel_frobenius(table.D[(r, 0)][1], B) < 1e-6
+
+
+# --------------------------------------------------------------------------
+# The tolerance metrics every parity verdict rests on, by hand
+# --------------------------------------------------------------------------
+
+def test_rel_frobenius_by_hand():
+    # ||(0, 0.5)|| / ||(3, 4)|| = 0.5 / 5
+    assert O.rel_frobenius([3.0, 4.5], [3.0, 4.0]) == pytest.approx(0.1, rel=1e-15)
+    # the norm is over every element of a matrix, not a row or a column:
+    # error (1, 2, 2) against reference (2, 0, 0, 4, 4) -> 3 / 6
+    a = np.array([[3.0, 2.0, 0.0], [6.0, 4.0, 0.0]])
+    ref = np.array([[2.0, 0.0, 0.0], [4.0, 4.0, 0.0]])
+    assert O.rel_frobenius(a, ref) == pytest.approx(0.5, rel=1e-15)
+    # the error's sign does not matter, and equal arrays give exactly 0
+    assert O.rel_frobenius([-1.0, 0.0], [1.0, 0.0]) == pytest.approx(2.0, rel=1e-15)
+    assert O.rel_frobenius(ref, ref) == 0.0
+    # an all-zero reference falls back to the absolute error norm
+    assert O.rel_frobenius([0.0, 3.0, 4.0], [0.0, 0.0, 0.0]) == pytest.approx(5.0, rel=1e-15)
+
+
+def test_max_rel_floor_by_hand():
+    ref = np.array([1.0, -2.0, 1e-3, 4.0])
+    rms = math.sqrt((1.0 + 4.0 + 1e-6 + 16.0) / 4.0)           # 2.29128...
+    floor = 1e-2 * rms
+    # one element off: |0.01| / |1|
+    assert O.max_rel_floor(ref + [0.01, 0, 0, 0], ref) == pytest.approx(0.01, rel=1e-12)
+    # an element below the floor is judged against the floor (0.0005 / 0.0229),
+    # not against its own magnitude (0.0005 / 0.001 = 0.5)
+    got = O.max_rel_floor(ref + [0, 0, 5e-4, 0], ref)
+    assert got == pytest.approx(5e-4 / floor, rel=1e-12)
+    assert got < 0.05
+    # the worst element decides, not the mean: errors 0.01/1 and 0.08/2 -> 0.04
+    assert O.max_rel_floor(ref + [0.01, 0.08, 0, 0], ref) == pytest.approx(0.04, rel=1e-12)
+    # a 2-D array is judged over all its elements with one rms
+    m = np.array([[1.0, 0.0], [0.0, -1.0]])                     # rms 1/sqrt(2)
+    err = np.array([[0.0, 1e-3], [0.0, 0.0]])                   # at a zero reference element
+    assert O.max_rel_floor(m + err, m) == pytest.approx(1e-3 / (1e-2 / math.sqrt(2.0)), rel=1e-12)
+    # an all-zero reference: rms 0, so the error is absolute; empty arrays give 0
+    assert O.max_rel_floor([0.0, 1e-3], [0.0, 0.0]) == pytest.approx(1e-3, rel=1e-15)
+    assert O.max_rel_floor([0.0, 0.0], [0.0, 0.0]) == 0.0
+    assert O.max_rel_floor(np.zeros(0), np.zeros(0)) == 0.0
+    # an explicit floor fraction is honoured
+    assert O.max_rel_floor(ref + [0, 0, 5e-4, 0], ref, floor_frac=0.1) == \
+        pytest.approx(5e-4 / (0.1 * rms), rel=1e-12)
