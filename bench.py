@@ -11,10 +11,14 @@ commits -- the whole hot path.  Every WRITE step also emits its token, so a
 step yields 8 tokens.
 
 Inputs are seeded synthetic tensors, resident in HBM before timing starts.
-The timed region is bracketed by torch.cuda.synchronize().  Each launch is
-also bracketed by HIP events on the launch stream; the READ kernel's average
-bandwidth over the timed region gives the roofline fraction.  The CPU oracle
-is then timed on a bounded sample of the same trace.
+The timed region is bracketed by torch.cuda.synchronize().  Runs of launches
+are also bracketed by HIP events on the launch stream; the READ kernel's
+average bandwidth over the timed region gives the roofline fraction.  The CPU
+oracle is then timed on a bounded sample of the same trace.  Finally a few
+steps of the other three workloads (8-owner READ-only, 32-owner ragged, 8B
+prefill then decode) are measured the same way and reported as compact
+records in the same line; the prefill workload's decode throughput is timed
+apart from its prefill WRITEs.
 """
 
 import argparse
@@ -141,6 +145,15 @@ class LaunchTimer:
         return self.torch.cuda.current_stream()
 
     def summary(self, wl, rank=0):
+        """Per call kind: launches, HIP-event time, algorithmic bytes and flops.
+
+        Algorithmic work follows the measurement plan: a READ of B owners moves
+        W0 once, each live state once, x and y; a WRITE of one owner reads its
+        live state, writes its shadow and reads Z and G, and does 2 C d_ff d_model
+        flops.  A WRITE step's token adds its x and y; its second read of W0
+        (and, where the token is not fused, of the live state) is reported as
+        ``token_extra_bytes``, not counted.
+        """
         K, N = wl.d_ff, wl.d_model
         io, st = wl.io_bytes, (4 if wl.state_dtype == "f32" else 2)
         out = {}
@@ -150,6 +163,7 @@ class LaunchTimer:
                 continue
             ms = sum(s.elapsed_time(e) for _, _, _, s, e, _ in recs)
             calls = sum(n for *_, n in recs)
+            extra = 0
             if rank:
                 # adapter: W0 once, each owner's A and B, x and y; WRITE reads the live
                 # factors, writes the shadow and reads Z and G
@@ -164,17 +178,39 @@ class LaunchTimer:
                 byt = sum(n * (K * N * (io + b * st) + b * io * (K + N)) for _, b, _, _, _, n in recs)
                 flop = sum(n * 4.0 * b * K * N for _, b, _, _, _, n in recs)
             else:
-                # live read + shadow write + Z, G; with the token also W0 once and x, y
                 tok = kind == "write_token"
-                byt = sum(n * (b * (2 * st * K * N + io * c * (K + N))
-                               + (K * N * io + b * io * (K + N) if tok else 0))
+                byt = sum(n * b * (2 * st * K * N + io * c * (K + N) + (io * (K + N) if tok else 0))
                           for _, b, c, _, _, n in recs)
-                flop = sum(n * (2.0 * b * c * K * N + (4.0 * b * K * N if tok else 0))
-                           for _, b, c, _, _, n in recs)
+                flop = sum(n * 2.0 * b * c * K * N for _, b, c, _, _, n in recs)
+                if tok:
+                    extra = sum(n * (K * N * io + (0 if fused_token(wl, c) else b * st * K * N))
+                                for _, b, c, _, _, n in recs)
+            by_chunk = {}
+            if kind != "read":
+                for c in sorted({r[2] for r in recs}):
+                    sub = [r for r in recs if r[2] == c]
+                    cms = sum(s.elapsed_time(e) for _, _, _, s, e, _ in sub)
+                    cn = sum(r[5] for r in sub)
+                    by_chunk[c] = dict(launches=cn, avg_us=1e3 * cms / cn,
+                                       owners=sum(r[1] * r[5] for r in sub) / cn)
             out[kind] = dict(launches=calls, total_ms=ms, avg_us=1e3 * ms / calls,
-                             bytes=byt, flops=flop, records=recs,
+                             bytes=byt, flops=flop, records=recs, token_extra_bytes=extra,
+                             by_chunk=by_chunk,
                              gbs=byt / (ms * 1e-3) / 1e9, tflops=flop / (ms * 1e-3) / 1e12)
         return out
+
+
+def fused_token(wl, chunk):
+    """Whether a WRITE with its token runs as one fused kernel (bf16 evidence, C <= 64)."""
+    return wl.io_dtype == "bf16" and chunk <= 64
+
+
+def write_kernel_name(wl, chunk, rank=0):
+    if rank:
+        return "adapter_pq_kernel+adapter_update_kernel"
+    if wl.io_dtype != "bf16":
+        return "write_valu_kernel"
+    return "write_stream_kernel" if chunk <= 64 else "write_gemm_kernel"
 
 
 def items_fn(wl):
@@ -243,17 +279,32 @@ def prepare(wl, layers, n_steps, threads, keep_layers, rank=0):
     return sess, X, Y, ZG, kept
 
 
-def run_gpu(args, wl, layers):
+def run_gpu(args, wl, layers, warmup, steps, keep=()):
+    """Run the workload's trace through the serving loop and time its windows.
+
+    A periodic schedule (READ-only, staggered) runs ``warmup`` untimed steps,
+    then one timed "decode" window of ``steps`` steps.  The ragged trace does
+    the same on its first warmup + steps steps.  The prefill-then-decode trace
+    runs once untimed, then again as two timed windows: "prefill" (the chunk
+    WRITEs, which emit no token) and "decode" (the READ steps), so decode
+    throughput never includes prefill time.  Each window is bracketed by
+    torch.cuda.synchronize() and has its own HIP-event launch timer.
+    """
     import torch
 
-    periodic = wl.schedule in ("staggered", "read_only")
-    # a periodic schedule runs warm-up steps then the timed steps; a finite one
-    # (ragged, prefill then decode) runs its whole trace once untimed, then again timed
-    n = args.warmup + args.steps if periodic else wl.n_steps
+    if wl.schedule in ("staggered", "read_only", "ragged"):
+        if wl.schedule == "ragged":
+            steps = max(1, min(steps, wl.n_steps - warmup))
+        n = warmup + steps
+        warm = range(warmup)
+        windows = [("decode", range(warmup, n))]
+    else:
+        n = wl.n_steps
+        warm = range(n)
+        windows = [("prefill", range(0, wl.n_prefill)), ("decode", range(wl.n_prefill, n))]
     t0 = time.time()
-    keep = set(args.cpu_layers) if args.cpu_baseline == "on" else set()
-    sess, X, Y, ZG, kept = prepare(wl, layers, n, args.threads, keep, args.rank)
-    log(f"setup {time.time() - t0:.1f} s")
+    sess, X, Y, ZG, kept = prepare(wl, layers, n, args.threads, set(keep), args.rank)
+    log(f"{wl.name}: setup {time.time() - t0:.1f} s")
     from paper_2605_28053_amd.serving import StreamPair
     if args.streams == 2:
         pair = StreamPair()
@@ -272,36 +323,42 @@ def run_gpu(args, wl, layers):
         res = sess.step(t, items, x_ptrs, y_ptrs, zg, sp, timer=timer)
         return sum(1 for it in items if it.emit), res
 
-    warm = range(args.warmup) if periodic else range(n)
-    timed = range(args.warmup, n) if periodic else range(n)
     for t in warm:
         one(t)
     torch.cuda.synchronize()
-    timer = LaunchTimer(torch, tstreams) if args.kernel_events == "on" else None
-    tokens = 0
-    writes = 0
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for t in timed:
-        k, res = one(t, timer)
-        tokens += k
-        writes += len(res.committed) + len(res.rolled_back)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
-    kern = timer.summary(wl, args.rank) if timer is not None else {}
+    out = {}
+    for label, rng in windows:
+        timer = LaunchTimer(torch, tstreams) if args.kernel_events == "on" else None
+        tokens = writes = 0
+        torch.cuda.synchronize()
+        t_start = time.perf_counter()
+        for t in rng:
+            k, res = one(t, timer)
+            tokens += k
+            writes += len(res.committed) + len(res.rolled_back)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t_start
+        out[label] = dict(tokens=tokens, elapsed=elapsed, writes=writes, steps=len(rng),
+                          kernels=timer.summary(wl, args.rank) if timer is not None else {})
     versions = sess.versions()
     sess.close()
-    return dict(tokens=tokens, elapsed=elapsed, kernels=kern, versions=versions,
-                writes=writes, kept=kept, steps=len(timed), warmup=len(warm))
+    return dict(windows=out, versions=versions, kept=kept, warmup=len(warm))
 
 
 def host_info():
     """The host the oracle ran on: logical CPUs, CPU model and memory."""
     info = {"nproc": os.cpu_count()}
     try:
+        # a virtualised host may name only the family: keep the family,
+        # model and stepping numbers and the clock beside the name
+        keys = {"model name": "cpu", "cpu family": "cpu_family", "model": "cpu_model",
+                "stepping": "cpu_stepping", "cpu MHz": "cpu_mhz"}
         for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                info["cpu"] = line.split(":", 1)[1].strip()
+            k, _, v = line.partition(":")
+            k = k.strip()
+            if k in keys and keys[k] not in info:
+                info[keys[k]] = v.strip()
+            if not line.strip() and "cpu" in info:
                 break
         for line in open("/proc/meminfo"):
             if line.startswith("MemTotal"):
@@ -483,6 +540,9 @@ def main():
                     help="2 (default): mixed8-4b-36L; 1 read8-4b; 3 ragged32-4b; 4 prefill8-8b")
     ap.add_argument("--rank", type=int, default=0,
                     help="0: fast-weight state (default); r > 0: the rank-r adapter backend")
+    ap.add_argument("--sub-workloads", choices=["on", "off"], default=None,
+                    help="also measure a few steps of workloads 1, 3 and 4 as compact records "
+                         "in the same line (default: on for workload 2)")
     ap.add_argument("--library-write", choices=["on", "off"], default="off",
                     help="also time torch.baddbmm (the vendor GEMM library) on the same "
                          "update as one WRITE call, for a bf16 state (context, not the value)")
@@ -522,20 +582,24 @@ def main():
     from rwttt_inputs import workload
     if args.cpu_baseline is None:
         args.cpu_baseline = "on" if args.workload == 2 else "off"
+    if args.sub_workloads is None:
+        args.sub_workloads = "on" if args.workload == 2 and not args.rank else "off"
     wl = workload(args.workload)
     layers = list(range(wl.n_layers if args.layers is None else args.layers))
 
-    g = run_gpu(args, wl, layers)
-    tok_s = g["tokens"] / g["elapsed"]
-    kern = g["kernels"]
+    g = run_gpu(args, wl, layers, args.warmup, args.steps,
+                keep=args.cpu_layers if args.cpu_baseline == "on" else ())
+    dec = g["windows"]["decode"]
+    tok_s = dec["tokens"] / dec["elapsed"]
+    kern = dec["kernels"]
     line = {
         "metric": METRIC,
         "value": round(tok_s, 2),
         "unit": "tok/s",
         "n_gpus": 1,
-        "steps": g["steps"],
+        "steps": dec["steps"],
         "warmup": g["warmup"],
-        "ms_per_step": round(1e3 * g["elapsed"] / g["steps"], 4),
+        "ms_per_step": round(1e3 * dec["elapsed"] / dec["steps"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -550,7 +614,8 @@ def main():
             "backend": f"delta_adapter rank {args.rank}" if args.rank else "fast_weight",
             "owners": wl.n_owners, "layers": len(layers), "d_model": wl.d_model, "d_ff": wl.d_ff,
             "io": wl.io_dtype, "state": wl.state_dtype, "accumulate": "f32",
-            "write_chunk": wl.chunk, "tokens_timed": g["tokens"], "writes_timed": g["writes"],
+            "write_chunk": wl.chunk or list(wl.chunk_choices),
+            "tokens_timed": dec["tokens"], "writes_timed": dec["writes"],
             "parallelism": "single-gpu",
             "streams": args.streams,
         },
@@ -567,26 +632,91 @@ def main():
                             "algorithmic_bytes_per_launch": round(rd["bytes"] / rd["launches"]),
                             "avg_launch_us": round(rd["avg_us"], 2),
                             "launches": rd["launches"]}
+    wk = write_record(wl, kern, args.rank)
+    if wk:
+        line["write_kernel"] = wk
+    if "prefill" in g["windows"]:
+        line["prefill"] = prefill_record(wl, g["windows"]["prefill"], args.rank)
     wkind = "write_token" if "write_token" in kern else "write"
-    if wkind in kern:
-        wr = kern[wkind]
-        wname = ("write_stream_kernel+read_reduce_kernel (token fused)" if wkind == "write_token"
-                 else "write update")
-        if args.rank:
-            wname = "adapter token read + adapter_pq_kernel + adapter_update_kernel"
-        line["write_kernel"] = {"kernel": wname,
-                                "achieved_gbs": round(wr["gbs"], 1),
-                                "hbm_frac": round(wr["gbs"] / HBM_PEAK_GBS, 4),
-                                "achieved_tflops": round(wr["tflops"], 2),
-                                "mfma_frac": round(wr["tflops"] / BF16_MFMA_PEAK_TFLOPS, 5),
-                                "avg_launch_us": round(wr["avg_us"], 2), "launches": wr["launches"]}
-    if args.library_write == "on" and wkind in kern:
-        line["library_write"] = time_library_write(torch, wl, kern[wkind])
+    if args.library_write == "on":
+        pk = g["windows"].get("prefill", dec)["kernels"]
+        pkind = "write" if "write" in pk else "write_token"
+        if pkind in pk:
+            line["library_write"] = time_library_write(torch, wl, pk[pkind])
     if args.cpu_baseline == "on":
         line["cpu_baseline"] = run_cpu_baseline(args, wl, g["kept"])
+    del g
+    if args.sub_workloads == "on":
+        line["workloads"] = {}
+        for wid, warm, steps in ((1, 3, 20), (3, 8, 40), (4, 0, 0)):
+            torch.cuda.empty_cache()
+            line["workloads"][workload(wid).name] = sub_record(args, workload(wid), warm, steps)
     line["paper_context"] = ("274.61 tok/s, 9.31x over sequential serving: full Qwen3-4B "
                              "In-Place-TTT model, 8 streams, one unnamed GPU (not this metric)")
     print(json.dumps(line), flush=True)
+
+
+def write_record(wl, kern, rank=0):
+    """The WRITE calls of a window: HBM fraction on algorithmic bytes (live read,
+    shadow write, Z, G, and a token's x and y), MFMA fraction on the update's
+    flops, and the token's second W0 read (plus its live read where not fused)
+    reported beside them."""
+    wkind = "write_token" if "write_token" in kern else "write"
+    if wkind not in kern:
+        return None
+    wr = kern[wkind]
+    chunks = sorted(wr["by_chunk"])
+    names = sorted({write_kernel_name(wl, c, rank) for c in chunks})
+    if wkind == "write_token" and not rank:
+        names.append("read_reduce_kernel (token)" if all(fused_token(wl, c) for c in chunks)
+                     else "READ launch (token)")
+    return {"kernel": "+".join(names),
+            "achieved_gbs": round(wr["gbs"], 1),
+            "hbm_frac": round(wr["gbs"] / HBM_PEAK_GBS, 4),
+            "achieved_tflops": round(wr["tflops"], 2),
+            "mfma_frac": round(wr["tflops"] / BF16_MFMA_PEAK_TFLOPS, 5),
+            "algorithmic_bytes_per_launch": round(wr["bytes"] / wr["launches"]),
+            "token_extra_bytes_per_launch": round(wr["token_extra_bytes"] / wr["launches"]),
+            "avg_launch_us": round(wr["avg_us"], 2), "launches": wr["launches"],
+            "by_chunk": {str(c): {"launches": v["launches"], "avg_us": round(v["avg_us"], 2),
+                                  "owners": round(v["owners"], 2)}
+                         for c, v in wr["by_chunk"].items()}}
+
+
+def prefill_record(wl, win, rank=0):
+    """The prefill window of a prefill-then-decode trace: chunk WRITEs with no token."""
+    rec = {"ms": round(1e3 * win["elapsed"], 3), "steps": win["steps"], "writes": win["writes"]}
+    wk = write_record(wl, win["kernels"], rank)
+    if wk:
+        rec["write_kernel"] = wk
+    return rec
+
+
+def sub_record(args, wl, warmup, steps):
+    """A compact record of one more workload: decode tok/s, READ and WRITE
+    fractions, and the prefill window where the workload has one."""
+    g = run_gpu(args, wl, list(range(wl.n_layers)), warmup, steps)
+    dec = g["windows"]["decode"]
+    rec = {"tok_s": round(dec["tokens"] / dec["elapsed"], 1), "steps": dec["steps"],
+           "warmup": g["warmup"], "tokens": dec["tokens"],
+           "ms_per_step": round(1e3 * dec["elapsed"] / dec["steps"], 4)}
+    kern = dec["kernels"]
+    if "read" in kern:
+        rd = kern["read"]
+        rec["read"] = {"frac": round(rd["gbs"] / HBM_PEAK_GBS, 4), "avg_us": round(rd["avg_us"], 2),
+                       "launches": rd["launches"],
+                       "owners": round(sum(r[1] * r[5] for r in rd["records"]) / rd["launches"], 2)}
+    wk = write_record(wl, kern, args.rank)
+    if wk:
+        rec["write"] = {k: wk[k] for k in ("kernel", "hbm_frac", "mfma_frac", "avg_launch_us",
+                                            "launches", "by_chunk")}
+    if "prefill" in g["windows"]:
+        pr = prefill_record(wl, g["windows"]["prefill"], args.rank)
+        rec["prefill"] = {"ms": pr["ms"], "writes": pr["writes"]}
+        if "write_kernel" in pr:
+            rec["prefill"].update({k: pr["write_kernel"][k] for k in
+                                   ("kernel", "mfma_frac", "hbm_frac", "avg_launch_us", "launches")})
+    return rec
 
 
 if __name__ == "__main__":

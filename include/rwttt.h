@@ -126,7 +126,9 @@ typedef struct rwttt_config {
 /* Bytes of device workspace a context with this config needs: the READ
  * split-K partial sums, n_owners x ceil(d_ff/256) x d_model fp32 values
  * (d_model rounded up to the column tile), and the fused WRITE token's
- * partial sums, n_owners x 48 x d_model fp32 values; for the adapter backend
+ * partial sums, n_owners x 64 x d_model fp32 values (one per row-tile
+ * partition of the streaming WRITE; the shape fixes at most 64 of them,
+ * d_model rounded up to 256); for the adapter backend
  * also n_owners x ceil(d_ff/256) x r partial sums of x A and two
  * n_owners x RWTTT_ADAPTER_MAX_CHUNK x r scratch matrices of a WRITE; one
  * region per owner.  Only the shape fields are read.  The workspace needs no
@@ -185,9 +187,18 @@ rwttt_status rwttt_plan(const rwttt_ctx* ctx, const rwttt_event* ev, uint32_t n_
  * their reduction).  Reads and writes of one context may run concurrently on
  * different streams when they name disjoint owners (the serving contract
  * gives each owner one transition per step); calls that share an owner must
- * be ordered on the device (same stream, or an event wait). */
+ * be ordered on the device (same stream, or an event wait).
+ *
+ * expected: NULL, or a host array indexed like owner_map (entry first+b
+ * belongs to slot b) holding the version each member was planned at
+ * (the event's v_i).  Every member must still be at it (Section 3, eq.
+ * compatibility: a group executes only members at their committed version);
+ * otherwise the call returns RWTTT_E_STALE_VERSION and launches nothing.
+ * The planner already guarantees this for a plan used in the same step;
+ * the check catches a group built by hand or kept across a commit. */
 rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
-                        uint32_t layer, const void* x, void* y, void* stream);
+                        const uint64_t* expected, uint32_t layer, const void* x, void* y,
+                        void* stream);
 
 /* Tail buffers (TailBufferState, Section 4.1; TailBufferUpdate, Section 4.2
  * primitives table and "READ"): request-local update evidence, the inputs x
@@ -207,9 +218,10 @@ rwttt_status rwttt_tail_len(const rwttt_ctx* ctx, uint32_t owner, uint32_t layer
  * of (owner, layer) at row tail_len, which then grows by one.  No version
  * changes (the tail is metadata, not a published state).  Errors, checked for
  * every owner before anything is launched: RWTTT_E_INVALID if no tail is
- * attached; RWTTT_E_CAPACITY if a tail is full. */
+ * attached; RWTTT_E_CAPACITY if a tail is full; `expected` as for rwttt_read. */
 rwttt_status rwttt_read_append(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
-                               uint32_t layer, const void* x, void* y, void* stream);
+                               const uint64_t* expected, uint32_t layer, const void* x, void* y,
+                               void* stream);
 
 /* WRITE / BoundaryUpdate (Section 3, Write; Section 4.2 "WRITE"): for each
  * slot b, owner r = owner_map[first+b]:
@@ -239,14 +251,15 @@ rwttt_status rwttt_read_append(rwttt_ctx* ctx, const rwttt_group* group, const u
  *
  * Marks each owner dirty (its write view is open until commit or rollback,
  * Section 4.1).  Errors: RWTTT_E_INVALID if only one of x, y is given;
- * RWTTT_E_DIRTY if this layer of an owner was already written in the open
- * transition.  If the launch fails (RWTTT_E_HIP) or a failure was injected
- * (RWTTT_E_WRITE_FAILED), the owners stay dirty and are marked failed: they
- * can only roll back. */
+ * RWTTT_E_STALE_VERSION if `expected` (as for rwttt_read) names a version
+ * other than V(r) for a member; RWTTT_E_DIRTY if this layer of an owner was
+ * already written in the open transition.  If the launch fails (RWTTT_E_HIP)
+ * or a failure was injected (RWTTT_E_WRITE_FAILED), the owners stay dirty and
+ * are marked failed: they can only roll back. */
 rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
-                         uint32_t layer, uint32_t chunk, const void* const* z,
-                         const void* const* g, float eta, const void* x, void* y,
-                         void* stream);
+                         const uint64_t* expected, uint32_t layer, uint32_t chunk,
+                         const void* const* z, const void* const* g, float eta, const void* x,
+                         void* y, void* stream);
 
 /* Commit (Section 4.2 CONTROL; Algorithm 1, CommitVersions): for each owner,
  * flip the live slot of every layer written in its open transition and set
@@ -265,7 +278,11 @@ rwttt_status rwttt_commit(rwttt_ctx* ctx, const uint32_t* owners, uint32_t n);
  * owners are accepted. */
 rwttt_status rwttt_rollback(rwttt_ctx* ctx, const uint32_t* owners, uint32_t n);
 
-/* View (Algorithm 1): committed version, and whether a candidate is open. */
+/* View (Algorithm 1): committed version, and whether a candidate is open.
+ * Either output pointer may be NULL.  Which slot is live is kept per (owner,
+ * layer), since a commit flips only the layers its transition wrote, so it
+ * is not an owner-wide value: rwttt_slot returns the live or shadow slot of
+ * one (owner, layer). */
 rwttt_status rwttt_version(const rwttt_ctx* ctx, uint32_t owner, uint64_t* version, int32_t* dirty);
 
 /* Device address of the live (which = 0) or shadow (which = 1) slot of

@@ -86,12 +86,12 @@ def _load():
         "rwttt_plan": (I32, [VP, P(rwttt_event), U32, U64, U32, U32,
                              P(rwttt_group), U32, P(U32), P(U32), U32, P(U32),
                              P(U32), U32, P(U32), P(I32)]),
-        "rwttt_read": (I32, [VP, P(rwttt_group), P(U32), U32, VP, VP, VP]),
-        "rwttt_read_append": (I32, [VP, P(rwttt_group), P(U32), U32, VP, VP, VP]),
+        "rwttt_read": (I32, [VP, P(rwttt_group), P(U32), P(U64), U32, VP, VP, VP]),
+        "rwttt_read_append": (I32, [VP, P(rwttt_group), P(U32), P(U64), U32, VP, VP, VP]),
         "rwttt_attach_tail": (I32, [VP, P(VP), U32]),
         "rwttt_tail_len": (I32, [VP, U32, U32, P(U32)]),
-        "rwttt_write": (I32, [VP, P(rwttt_group), P(U32), U32, U32, P(VP), P(VP), C.c_float,
-                              VP, VP, VP]),
+        "rwttt_write": (I32, [VP, P(rwttt_group), P(U32), P(U64), U32, U32, P(VP), P(VP),
+                              C.c_float, VP, VP, VP]),
         "rwttt_commit": (I32, [VP, P(U32), U32]),
         "rwttt_rollback": (I32, [VP, P(U32), U32]),
         "rwttt_version": (I32, [VP, U32, P(U64), P(I32)]),
@@ -210,15 +210,23 @@ def rwttt_plan(ctx, events, step, target_b=0, wait_budget=0, cap=None):
     return PlanResult(st, groups, ng.value, omap, nm.value, defer, nd.value, st_arr[:n])
 
 
-def rwttt_read(ctx, group, owner_map, layer, x_ptr, y_ptr, stream=0):
-    """``group``: rwttt_group (or pointer); ``owner_map``: ctypes uint32 array."""
-    return _lib.rwttt_read(ctx, C.byref(group), owner_map, int(layer), int(x_ptr), int(y_ptr),
-                           int(stream) or None)
+def _u64_or_null(seq):
+    if seq is None or isinstance(seq, C.Array):
+        return seq
+    seq = list(seq)
+    return (C.c_uint64 * max(1, len(seq)))(*seq)
 
 
-def rwttt_read_append(ctx, group, owner_map, layer, x_ptr, y_ptr, stream=0):
-    return _lib.rwttt_read_append(ctx, C.byref(group), owner_map, int(layer), int(x_ptr),
-                                  int(y_ptr), int(stream) or None)
+def rwttt_read(ctx, group, owner_map, layer, x_ptr, y_ptr, stream=0, expected=None):
+    """``group``: rwttt_group (or pointer); ``owner_map``: ctypes uint32 array;
+    ``expected``: None or the planned versions, indexed like ``owner_map``."""
+    return _lib.rwttt_read(ctx, C.byref(group), owner_map, _u64_or_null(expected), int(layer),
+                           int(x_ptr), int(y_ptr), int(stream) or None)
+
+
+def rwttt_read_append(ctx, group, owner_map, layer, x_ptr, y_ptr, stream=0, expected=None):
+    return _lib.rwttt_read_append(ctx, C.byref(group), owner_map, _u64_or_null(expected),
+                                  int(layer), int(x_ptr), int(y_ptr), int(stream) or None)
 
 
 def rwttt_attach_tail(ctx, tail_ptrs, rows):
@@ -235,14 +243,15 @@ def rwttt_tail_len(ctx, owner, layer):
 
 
 def rwttt_write(ctx, group, owner_map, layer, chunk, z_ptrs, g_ptrs, eta, x_ptr=0, y_ptr=0,
-                stream=0):
+                stream=0, expected=None):
     """x_ptr/y_ptr: the WRITE step's owner-indexed token input/output (0: no token).
-    z_ptrs=None: the chunk is the owners' tails plus this step's x."""
+    z_ptrs=None: the chunk is the owners' tails plus this step's x.
+    expected: None or the planned versions, indexed like ``owner_map``."""
     n = len(g_ptrs)
     z = None if z_ptrs is None else (C.c_void_p * max(1, n))(*[int(p) for p in z_ptrs])
     g = (C.c_void_p * max(1, n))(*[int(p) for p in g_ptrs])
-    return _lib.rwttt_write(ctx, C.byref(group), owner_map, int(layer), int(chunk), z, g,
-                            float(eta), int(x_ptr) or None, int(y_ptr) or None,
+    return _lib.rwttt_write(ctx, C.byref(group), owner_map, _u64_or_null(expected), int(layer),
+                            int(chunk), z, g, float(eta), int(x_ptr) or None, int(y_ptr) or None,
                             int(stream) or None)
 
 
@@ -303,3 +312,8 @@ def make_group(effect, first, count, backend_type=0, shape_class=0, placement=0)
 
 def u32_array(seq):
     return _u32(seq)[0]
+
+
+def u64_array(seq):
+    seq = list(seq)
+    return (C.c_uint64 * max(1, len(seq)))(*seq)

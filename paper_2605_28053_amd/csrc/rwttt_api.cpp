@@ -286,8 +286,18 @@ rwttt_status rwttt_plan(const rwttt_ctx* ctx, const rwttt_event* ev, uint32_t n_
 
 namespace {
 
+// Defence in depth beside the planner (Section 3, eq. compatibility): every
+// member must still be at the version the caller planned it at.
+bool versions_match(const rwttt_ctx* ctx, const uint32_t* owners, const uint64_t* expected, uint32_t n) {
+  if (!expected) return true;
+  for (uint32_t b = 0; b < n; ++b)
+    if (expected[b] != ctx->version[owners[b]]) return false;
+  return true;
+}
+
 rwttt_status read_impl(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
-                       uint32_t layer, const void* x, void* y, void* stream, bool append) {
+                       const uint64_t* expected, uint32_t layer, const void* x, void* y, void* stream,
+                       bool append) {
   if (!ctx || !group) return RWTTT_E_INVALID;
   if (group->effect != RWTTT_READ && group->effect != RWTTT_WRITE) return RWTTT_E_INVALID;
   const uint32_t n = group->count;
@@ -297,6 +307,8 @@ rwttt_status read_impl(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t*
   const uint32_t* owners = owner_map + group->first;
   rwttt_status why = RWTTT_OK;
   if (!ctx->distinct_owners(owners, n, &why)) return why;
+  if (!versions_match(ctx, owners, expected ? expected + group->first : nullptr, n))
+    return RWTTT_E_STALE_VERSION;
   if (!ctx->cfg.workspace) return RWTTT_E_INVALID;
   if (append) {
     if (ctx->tail.empty() || !aligned16(x)) return RWTTT_E_INVALID;
@@ -357,13 +369,14 @@ rwttt_status read_impl(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t*
 }  // namespace
 
 rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
-                        uint32_t layer, const void* x, void* y, void* stream) {
-  return read_impl(ctx, group, owner_map, layer, x, y, stream, false);
+                        const uint64_t* expected, uint32_t layer, const void* x, void* y, void* stream) {
+  return read_impl(ctx, group, owner_map, expected, layer, x, y, stream, false);
 }
 
 rwttt_status rwttt_read_append(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
-                               uint32_t layer, const void* x, void* y, void* stream) {
-  return read_impl(ctx, group, owner_map, layer, x, y, stream, true);
+                               const uint64_t* expected, uint32_t layer, const void* x, void* y,
+                               void* stream) {
+  return read_impl(ctx, group, owner_map, expected, layer, x, y, stream, true);
 }
 
 rwttt_status rwttt_attach_tail(rwttt_ctx* ctx, void* const* tail, uint32_t rows) {
@@ -384,8 +397,8 @@ rwttt_status rwttt_tail_len(const rwttt_ctx* ctx, uint32_t owner, uint32_t layer
 }
 
 rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
-                         uint32_t layer, uint32_t chunk, const void* const* z, const void* const* g,
-                         float eta, const void* x, void* y, void* stream) {
+                         const uint64_t* expected, uint32_t layer, uint32_t chunk, const void* const* z,
+                         const void* const* g, float eta, const void* x, void* y, void* stream) {
   if (!ctx || !group) return RWTTT_E_INVALID;
   if (group->effect != RWTTT_WRITE) return RWTTT_E_KEY_MISMATCH;
   const uint32_t n = group->count;
@@ -401,6 +414,8 @@ rwttt_status rwttt_write(rwttt_ctx* ctx, const rwttt_group* group, const uint32_
   const uint32_t* owners = owner_map + group->first;
   rwttt_status why = RWTTT_OK;
   if (!ctx->distinct_owners(owners, n, &why)) return why;
+  if (!versions_match(ctx, owners, expected ? expected + group->first : nullptr, n))
+    return RWTTT_E_STALE_VERSION;
   for (uint32_t b = 0; b < n; ++b) {
     if (!g[b] || !aligned16(g[b])) return RWTTT_E_INVALID;
     if (!from_tail && (!z[b] || !aligned16(z[b]))) return RWTTT_E_INVALID;

@@ -203,9 +203,14 @@ class Session:
         s_write = pair.write if pair else stream
         wl = self.wl
         by_owner = {it.owner: it for it in items}
-        plan = R.rwttt_plan(self.ctx, self.events(t, items), t)
+        evs = self.events(t, items)
+        plan = R.rwttt_plan(self.ctx, evs, t)
         if plan.status != R.RWTTT_OK:
             raise R.RwtttError(plan.status, "rwttt_plan")
+        # the version each member was planned at, indexed like the owner map:
+        # every read and write re-checks it against the owner table
+        planned = {e[0]: e[5] for e in evs}
+        expected = R.u64_array(planned[plan.owner_map_c[i]] for i in range(plan.n_mapped))
         statuses = []
         write_groups = []
         for gi in range(plan.n_groups):
@@ -227,7 +232,7 @@ class Session:
                         timer.launch("write_token" if tok else "write", g.count, chunk, stream)
                     st = R.rwttt_write(self.ctx, g, plan.owner_map_c, i, chunk, zs, gs, wl.eta,
                                        x_ptrs[i] if tok else 0, y_ptrs[i] if tok else 0,
-                                       stream)
+                                       stream, expected)
                     statuses.append(st)
                     if st == R.RWTTT_OK:
                         need_token = False
@@ -240,7 +245,7 @@ class Session:
                     if timer is not None:
                         timer.launch("read", g.count, 0, stream)
                     fn = R.rwttt_read_append if self.tails and not is_write else R.rwttt_read
-                    st = fn(self.ctx, g, plan.owner_map_c, i, x_ptrs[i], y_ptrs[i], stream)
+                    st = fn(self.ctx, g, plan.owner_map_c, i, x_ptrs[i], y_ptrs[i], stream, expected)
                     if st != R.RWTTT_OK:
                         raise R.RwtttError(st, "rwttt_read")
             if is_write:

@@ -60,7 +60,11 @@ int main(void) {
   CHECK(rwttt_inject_write_failures(ctx, 1) == RWTTT_OK);
   const void* z[1] = {(const void*)0x100};
   const void* g[1] = {(const void*)0x200};
-  CHECK(rwttt_write(ctx, &groups[1], omap, 0, 4, z, g, 1.0f, NULL, NULL, NULL) == RWTTT_E_WRITE_FAILED);
+  /* a member planned at a version other than V(r) is refused before anything changes */
+  const uint64_t stale[4] = {0, 0, 0, 1};
+  CHECK(rwttt_write(ctx, &groups[1], omap, stale, 0, 4, z, g, 1.0f, NULL, NULL, NULL) == RWTTT_E_STALE_VERSION);
+  const uint64_t planned[4] = {0, 0, 0, 0};
+  CHECK(rwttt_write(ctx, &groups[1], omap, planned, 0, 4, z, g, 1.0f, NULL, NULL, NULL) == RWTTT_E_WRITE_FAILED);
   uint64_t v = 99;
   int32_t dirty = 0;
   CHECK(rwttt_version(ctx, 2, &v, &dirty) == RWTTT_OK && v == 0 && dirty == 1);
@@ -71,7 +75,11 @@ int main(void) {
   CHECK(rwttt_version(ctx, 2, &v, &dirty) == RWTTT_OK && v == 0 && dirty == 0);
 
   /* a host-only context refuses device work */
-  CHECK(rwttt_read(ctx, &groups[0], omap, 0, (const void*)0x1000, (void*)0x2000, NULL) == RWTTT_E_INVALID);
+  CHECK(rwttt_read(ctx, &groups[0], omap, NULL, 0, (const void*)0x1000, (void*)0x2000, NULL) == RWTTT_E_INVALID);
+  CHECK(rwttt_read(ctx, &groups[0], omap, stale, 0, (const void*)0x1000, (void*)0x2000, NULL) == RWTTT_E_INVALID);
+  const uint64_t stale_read[4] = {0, 5, 0, 0};
+  CHECK(rwttt_read(ctx, &groups[0], omap, stale_read, 0, (const void*)0x1000, (void*)0x2000, NULL) ==
+        RWTTT_E_STALE_VERSION);
   CHECK(rwttt_fork(ctx, 0, 1, NULL) == RWTTT_E_INVALID);
   CHECK(strlen(rwttt_strerror(RWTTT_E_STALE_VERSION)) > 0);
 

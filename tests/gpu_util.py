@@ -59,9 +59,10 @@ def host_f64(t, dtype):
 
 
 def run_gpu_trace(wl, trace, src, steps, layers=None, cols=None, fail_hook=None, stream=None,
-                  backend=0, rank=0):
+                  backend=0, rank=0, on_step=None):
     """Run steps of a trace through Session.step (the serving loop) and collect
-    (StepResult, versions after the step, {(owner, layer): y row}) per step."""
+    (StepResult, versions after the step, {(owner, layer): y row}) per step.
+    ``on_step(sess, t)`` runs after each step, once the device is idle."""
     layers = list(range(wl.n_layers)) if layers is None else list(layers)
     sess = Session(wl, src, layers, backend=backend, rank=rank)
     out = []
@@ -93,6 +94,8 @@ def run_gpu_trace(wl, trace, src, steps, layers=None, cols=None, fail_hook=None,
                     row = host_f64(Y[i][it.owner], wl.io_dtype)
                     ys[(it.owner, l)] = row if cols is None else row[cols]
         out.append((res, sess.versions(), ys))
+        if on_step is not None:
+            on_step(sess, t)
     return sess, out
 
 

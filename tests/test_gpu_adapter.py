@@ -50,6 +50,7 @@ READ_CASES = [
     (9728, 2560, "bf16", "f32", 8, 8, list(range(8))),
     # rank above 8 (a second u-share pass) that is not a power of two
     (3000, 2600, "bf16", "f32", 12, 9, [7, 2, 8, 0, 5, 1, 3, 4, 6]),
+    (520, 264, "f32", "bf16", 4, 3, [2, 0]),          # fp32 io, bf16 factors
 ]
 
 
@@ -99,6 +100,7 @@ WRITE_CASES = [
     (2104, 1096, "bf16", "f32", 5, 33, [2, 0]),
     (2104, 1096, "bf16", "bf16", 12, 70, [3]),
     (1000, 264, "f32", "f32", 16, 20, [1, 2]),
+    (520, 264, "f32", "bf16", 4, 6, [1, 2]),          # fp32 evidence into bf16 factors
 ]
 
 

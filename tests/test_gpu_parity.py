@@ -124,6 +124,9 @@ WRITE_CASES = [
     (9728, 2560, "bf16", "f32", 64, [1]),
     (264, 136, "bf16", "f32", 33, [11, 4, 0, 7, 2, 9, 5, 1, 10, 3, 8, 6]),   # 12 owners, stream path
     (264, 136, "bf16", "bf16", 130, [9, 2, 5, 0, 7, 3, 8, 1, 6, 4]),        # 10 owners, GEMM path
+    (264, 520, "f32", "bf16", 5, [1, 0]),              # fp32 evidence into bf16 state (VALU path)
+    (2056, 264, "bf16", "bf16", 64, [2, 0]),           # 65 row tiles over 33 partitions of 2 and 1 items
+    (3080, 264, "bf16", "f32", 48, [0, 2, 1]),         # 97 row tiles over 49 partitions of 2 and 1 items
 ]
 
 
@@ -182,7 +185,10 @@ TOKEN_CASES = [
     (40, 24, "bf16", "f32", 1, [2], 3),               # one row tile, one partition
     (1000, 264, "bf16", "f32", 17, [0, 3, 1], 4),     # ragged rows and columns
     (1000, 264, "bf16", "bf16", 64, [1, 2], 4),
-    (1576, 520, "bf16", "f32", 64, [4, 0, 2], 5),     # 50 row tiles over 48 partitions
+    (1576, 520, "bf16", "f32", 64, [4, 0, 2], 5),     # 50 row tiles, one per partition
+    (2056, 264, "bf16", "bf16", 64, [2, 0, 3], 4),    # bf16 state, partitions of 2 and 1 items
+    (3080, 264, "bf16", "f32", 48, [1, 0], 3),        # fp32 state, partitions of 2 and 1 items
+    (264, 520, "f32", "bf16", 5, [1, 0], 2),          # fp32 evidence, bf16 state: READ, then VALU
     (520, 1032, "bf16", "f32", 100, [3, 0], 4),       # large chunk: READ, then the GEMM
     (256, 64, "f32", "f32", 4, [0, 1], 2),            # fp32 evidence
     (9728, 2560, "bf16", "f32", 64, [5, 1, 7], 8),    # full 4B-layer shape

@@ -33,14 +33,37 @@ def sample_cols(wl, n=64, seed=5):
     return np.sort(np.concatenate([[0, wl.d_model - 1], inner]))
 
 
-def check_trace(wl, steps, layers, n_cols=64, threads=16):
+def check_trace(wl, steps, layers, n_cols=64, threads=16, snap_version=None):
+    """With ``snap_version`` = k, every owner's state is also compared when its
+    committed version first reaches k (returns how many owners were)."""
     src = TensorSource(wl, memo=True)
     src.prefetch(range(wl.n_owners), layers, threads)
     trace = build_trace(wl, max(steps) + 1)
     cols = sample_cols(wl, n_cols)
-    ref, table = O.run_trace(wl, trace, src, steps=steps, layers=layers, cols=cols)
+    ref_snap, gpu_snap = {}, {}
+
+    def oracle_snap(rec, table):
+        for r in range(wl.n_owners):
+            if table.V[r] == snap_version and r not in ref_snap:
+                ref_snap[r] = (rec.step, [table.D[(r, l)].copy() for l in layers])
+
+    def gpu_snap_at(sess, t):
+        for r, v in enumerate(sess.versions()):
+            if v == snap_version and r not in gpu_snap:
+                gpu_snap[r] = (t, [host_f64(sess.live(r, i), wl.state_dtype)[:, cols]
+                                   for i in range(len(layers))])
+
+    ref, table = O.run_trace(wl, trace, src, steps=steps, layers=layers, cols=cols,
+                             on_step=oracle_snap if snap_version else None)
     say("oracle done", wl.name)
-    sess, got = run_gpu_trace(wl, trace, src, steps, layers=layers, cols=cols)
+    sess, got = run_gpu_trace(wl, trace, src, steps, layers=layers, cols=cols,
+                              on_step=gpu_snap_at if snap_version else None)
+    assert set(gpu_snap) == set(ref_snap)
+    for r, (t, states) in ref_snap.items():
+        assert gpu_snap[r][0] == t, r
+        for i, l in enumerate(layers):
+            err = O.rel_frobenius(gpu_snap[r][1][i], states[i])
+            assert err <= STATE_TOL, (r, l, t, err)
     n_writes = n_fail = 0
     for rec, (res, versions, ys) in zip(ref, got):
         assert plan_tuples(res) == [(g.key, g.owners) for g in rec.plan.groups], rec.step
@@ -61,29 +84,33 @@ def check_trace(wl, steps, layers, n_cols=64, threads=16):
             assert err <= STATE_TOL, (r, l, err)
     say(wl.name, "writes", n_writes, "rolled back", n_fail, "worst state error", worst)
     sess.close()
-    return n_writes, n_fail, table
+    return n_writes, n_fail, table, len(ref_snap)
 
 
 def test_mixed36_bench_workload_sampled():
     """The bench workload: 8 streams, C=64 WRITEs at steps 8 and 16; first and last layer."""
     wl = workload(2)
-    n_writes, n_fail, table = check_trace(wl, range(18), layers=[0, 35])
+    n_writes, n_fail, table, _ = check_trace(wl, range(18), layers=[0, 35])
     assert n_writes == 2 and n_fail == 0
     assert table.V == [0, 0, 0, 0, 0, 0, 1, 1]
 
 
 def test_ragged32_sampled():
-    """32 owners, shuffled events, C in {16,32,64}, injected failures rolled back."""
+    """32 owners, shuffled events, C in {16,32,64}, injected failures rolled back.
+    Every owner is also checked at the step its 16th WRITE commits (fp32 state
+    within 1e-3 relative Frobenius after 16 writes): 20 owners get there within
+    72 steps."""
     wl = workload(3)
-    n_writes, n_fail, table = check_trace(wl, range(48), layers=[0])
-    assert n_writes == 48 * 8 and n_fail > 0
+    n_writes, n_fail, table, n16 = check_trace(wl, range(72), layers=[0], snap_version=16)
+    assert n_writes == 72 * 8 and n_fail > 0
     assert sum(table.V) == n_writes - n_fail
+    assert n16 == 20
 
 
 def test_prefill8b_bf16_state_sampled():
     """8B-class shape, bf16 state from zero: 8 prefill C=512 WRITE groups, then decode."""
     wl = workload(4)
-    n_writes, n_fail, table = check_trace(wl, range(12), layers=[0])
+    n_writes, n_fail, table, _ = check_trace(wl, range(12), layers=[0])
     assert n_writes == 64 and n_fail == 0
     assert table.V == [8] * 8
 

@@ -139,6 +139,30 @@ def test_owner_table_state_machine_and_error_codes():
     assert R.rwttt_read(ctx, ag, R.u32_array([2, 2]), 0, 0x1000, 0x2000) == R.RWTTT_E_OWNER_ALIAS
 
 
+def test_read_and_write_recheck_planned_versions():
+    """Each member's planned version is checked against V(r) before anything
+    changes (Section 3, eq. compatibility); `expected` is indexed like the owner
+    map, so a group in the middle of the map reads its own entries."""
+    ctx, _ = host_ctx(n_owners=4)                          # every V(r) is 0
+    omap = R.u32_array([3, 2, 0])
+    rg = R.make_group(R.RWTTT_READ, 1, 2)                  # members 2, 0
+    stale = [9, 1, 0]                                       # owner 2 is at 0, not 1
+    assert R.rwttt_read(ctx, rg, omap, 0, 0x1000, 0x2000, expected=stale) == R.RWTTT_E_STALE_VERSION
+    assert R.rwttt_read_append(ctx, rg, omap, 0, 0x1000, 0x2000, expected=stale) == \
+        R.RWTTT_E_STALE_VERSION
+    wg = R.make_group(R.RWTTT_WRITE, 1, 2)
+    assert R.rwttt_write(ctx, wg, omap, 0, 4, [0x100] * 2, [0x200] * 2, 1.0,
+                         expected=stale) == R.RWTTT_E_STALE_VERSION
+    assert [R.rwttt_version(ctx, r) for r in range(4)] == [(0, False)] * 4
+    # entry 0 belongs to owner 3, which is not in the group: its value is not read
+    ok = [9, 0, 0]
+    assert R.rwttt_read(ctx, rg, omap, 0, 0x1000, 0x2000, expected=ok) == R.RWTTT_E_INVALID  # host-only
+    assert R.rwttt_inject_write_failures(ctx, 1) == R.RWTTT_OK
+    assert R.rwttt_write(ctx, wg, omap, 0, 4, [0x100] * 2, [0x200] * 2, 1.0,
+                         expected=ok) == R.RWTTT_E_WRITE_FAILED
+    assert R.rwttt_version(ctx, 2) == (0, True) and R.rwttt_version(ctx, 0) == (0, True)
+
+
 def test_tail_state_machine_and_errors_before_any_launch():
     """Tail validation paths that return before the device is touched: the
     workspace address below is never dereferenced."""
