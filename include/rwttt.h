@@ -200,6 +200,29 @@ rwttt_status rwttt_read(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t
                         const uint64_t* expected, uint32_t layer, const void* x, void* y,
                         void* stream);
 
+/* Largest device scratch rwttt_read_noalloc uses: its static array's size. */
+#define RWTTT_NOALLOC_SCRATCH_BYTES (16u << 20)
+
+/* rwttt_read for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  The
+ * same computation, kernels and results as rwttt_read (bit for bit), but the
+ * split-K partial sums go to a static device array of
+ * RWTTT_NOALLOC_SCRATCH_BYTES inside the library instead of the context's
+ * workspace, so the context may be a host-only one (workspace NULL).  The
+ * call allocates and frees nothing.  A group needs
+ * count x ceil(d_ff/256) x d_model fp32 values of the array (d_model rounded
+ * up to the column tile: 256 for fp32 state, 512 for bf16 state); a larger
+ * group returns RWTTT_E_CAPACITY.  Fast-weight backend only (RWTTT_E_INVALID
+ * for an adapter context); no tail append.  The stream must belong to the
+ * current device: each GPU holds its own copy of the array (until the process
+ * ends), found on the first call with that device current.  Every call on a
+ * GPU shares that GPU's array: calls that overlap on one GPU (other streams,
+ * other contexts, other host threads) race and give wrong results.  Other
+ * errors as for rwttt_read. */
+rwttt_status rwttt_read_noalloc(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
+                                const uint64_t* expected, uint32_t layer, const void* x, void* y,
+                                void* stream);
+
 /* Tail buffers (TailBufferState, Section 4.1; TailBufferUpdate, Section 4.2
  * primitives table and "READ"): request-local update evidence, the inputs x
  * of the steps since the owner's last update boundary, kept for the next

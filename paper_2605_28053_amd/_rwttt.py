@@ -31,6 +31,7 @@ RWTTT_FAST_WEIGHT = 0
 RWTTT_DELTA_ADAPTER = 1
 RWTTT_MAX_RANK = 32
 RWTTT_ADAPTER_MAX_CHUNK = 1024
+RWTTT_NOALLOC_SCRATCH_BYTES = 16 << 20
 
 
 class rwttt_event(C.Structure):
@@ -88,6 +89,7 @@ def _load():
                              P(U32), U32, P(U32), P(I32)]),
         "rwttt_read": (I32, [VP, P(rwttt_group), P(U32), P(U64), U32, VP, VP, VP]),
         "rwttt_read_append": (I32, [VP, P(rwttt_group), P(U32), P(U64), U32, VP, VP, VP]),
+        "rwttt_read_noalloc": (I32, [VP, P(rwttt_group), P(U32), P(U64), U32, VP, VP, VP]),
         "rwttt_attach_tail": (I32, [VP, P(VP), U32]),
         "rwttt_tail_len": (I32, [VP, U32, U32, P(U32)]),
         "rwttt_write": (I32, [VP, P(rwttt_group), P(U32), P(U64), U32, U32, P(VP), P(VP),
@@ -227,6 +229,11 @@ def rwttt_read(ctx, group, owner_map, layer, x_ptr, y_ptr, stream=0, expected=No
 def rwttt_read_append(ctx, group, owner_map, layer, x_ptr, y_ptr, stream=0, expected=None):
     return _lib.rwttt_read_append(ctx, C.byref(group), owner_map, _u64_or_null(expected),
                                   int(layer), int(x_ptr), int(y_ptr), int(stream) or None)
+
+
+def rwttt_read_noalloc(ctx, group, owner_map, layer, x_ptr, y_ptr, stream=0, expected=None):
+    return _lib.rwttt_read_noalloc(ctx, C.byref(group), owner_map, _u64_or_null(expected),
+                                   int(layer), int(x_ptr), int(y_ptr), int(stream) or None)
 
 
 def rwttt_attach_tail(ctx, tail_ptrs, rows):

@@ -379,6 +379,47 @@ rwttt_status rwttt_read_append(rwttt_ctx* ctx, const rwttt_group* group, const u
   return read_impl(ctx, group, owner_map, expected, layer, x, y, stream, true);
 }
 
+rwttt_status rwttt_read_noalloc(rwttt_ctx* ctx, const rwttt_group* group, const uint32_t* owner_map,
+                                const uint64_t* expected, uint32_t layer, const void* x, void* y,
+                                void* stream) {
+  if (!ctx || !group) return RWTTT_E_INVALID;
+  if (group->effect != RWTTT_READ && group->effect != RWTTT_WRITE) return RWTTT_E_INVALID;
+  if (is_adapter(&ctx->cfg)) return RWTTT_E_INVALID;
+  const uint32_t n = group->count;
+  if (n == 0) return RWTTT_OK;
+  if (!owner_map || !x || !y || layer >= ctx->cfg.n_layers) return RWTTT_E_INVALID;
+  if (n > ctx->cfg.max_group) return RWTTT_E_CAPACITY;
+  const uint32_t* owners = owner_map + group->first;
+  rwttt_status why = RWTTT_OK;
+  if (!ctx->distinct_owners(owners, n, &why)) return why;
+  if (!versions_match(ctx, owners, expected ? expected + group->first : nullptr, n))
+    return RWTTT_E_STALE_VERSION;
+  const int state_bf16 = ctx->cfg.state_dtype == RWTTT_BF16;
+  if (rwttt::read_noalloc_bytes(int(ctx->cfg.d_ff), int(ctx->cfg.d_model), state_bf16, int(n)) >
+      RWTTT_NOALLOC_SCRATCH_BYTES)
+    return RWTTT_E_CAPACITY;
+
+  rwttt::ReadLaunch L;
+  L.io_bf16 = ctx->cfg.io_dtype == RWTTT_BF16;
+  L.state_bf16 = state_bf16;
+  L.d_ff = int(ctx->cfg.d_ff);
+  L.d_model = int(ctx->cfg.d_model);
+  L.count = int(n);
+  L.n_owners = int(ctx->cfg.n_owners);
+  L.x = x;
+  L.y = y;
+  L.w0 = ctx->w0[layer];
+  L.workspace = nullptr;
+  for (uint32_t b = 0; b < n; ++b) {
+    L.dw[b] = ctx->slot(owners[b], layer, 0);
+    L.row[b] = owners[b];
+    L.tail[b] = nullptr;
+  }
+  const hipError_t e = rwttt::launch_read_noalloc(L, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(ctx, e);
+  return RWTTT_OK;
+}
+
 rwttt_status rwttt_attach_tail(rwttt_ctx* ctx, void* const* tail, uint32_t rows) {
   if (!ctx || !tail || rows == 0 || rows > (1u << 20)) return RWTTT_E_INVALID;
   const size_t nl = size_t(ctx->cfg.n_owners) * ctx->cfg.n_layers;

@@ -69,6 +69,13 @@ struct WriteLaunch {
 };
 
 hipError_t launch_read(const ReadLaunch& L, hipStream_t stream);
+
+// The same READ with its partial sums in the library's static device array
+// (one region per group slot; L.workspace and L.n_owners are not used for
+// them).  Allocates nothing.  read_noalloc_bytes() is the array space a call
+// needs; a call above RWTTT_NOALLOC_SCRATCH_BYTES returns hipErrorInvalidValue.
+size_t read_noalloc_bytes(int d_ff, int d_model, int state_bf16, int count);
+hipError_t launch_read_noalloc(const ReadLaunch& L, hipStream_t stream);
 hipError_t launch_tail_append(const TailLaunch& L, hipStream_t stream);
 
 // ---- DeltaAdapterState backend (rwttt_adapter.hip) ----

@@ -6,6 +6,7 @@
 // Both operate on groups of owners, one launch per (group, layer).
 
 #include <algorithm>
+#include <mutex>
 
 #include "rwttt_kernels.h"
 
@@ -47,6 +48,7 @@ struct ReadParams {
   const void* w0;
   float* part;
   int count, d_ff, d_model, ks, nt, npad;
+  int slot_part;             // partial sums indexed by group slot (1) or by owner id (0)
   const void* dw[RWTTT_MAX_GROUP];
   uint32_t row[RWTTT_MAX_GROUP];
   void* tail[RWTTT_MAX_GROUP];     // TailBufferUpdate: row receiving x, or null
@@ -122,7 +124,8 @@ __global__ void __launch_bounds__(kReadThreads) read_partial_kernel(const ReadPa
 #pragma unroll
   for (int c = 0; c < COLS; ++c) red[wave][lane * COLS + c] = acc[c];
   __syncthreads();
-  float* dst = p.part + (size_t(p.row[b]) * p.ks + kc) * p.npad + nt * TILE_N;
+  const uint32_t prow = p.slot_part ? uint32_t(b) : p.row[b];
+  float* dst = p.part + (size_t(prow) * p.ks + kc) * p.npad + nt * TILE_N;
   for (int j = tid; j < TILE_N; j += kReadThreads)
     dst[j] = ((red[0][j] + red[1][j]) + red[2][j]) + red[3][j];
 }
@@ -143,7 +146,8 @@ __global__ void __launch_bounds__(256) read_reduce_kernel(const ReadParams p) {
   const int k0 = wave * per, k1 = min(p.ks, k0 + per);
   float s = 0.f;
   if (n < p.d_model) {
-    const float* q = p.part + size_t(p.row[b]) * p.ks * p.npad + n;
+    const uint32_t prow = p.slot_part ? uint32_t(b) : p.row[b];
+    const float* q = p.part + size_t(prow) * p.ks * p.npad + n;
     for (int k = k0; k < k1; k += kRedBatch) {
       float a[kRedBatch];
 #pragma unroll
@@ -855,13 +859,14 @@ __global__ void __launch_bounds__(256) copy_kernel(const CopyParams p) {
 }
 
 template <typename IO, typename ST>
-hipError_t launch_read_t(const ReadLaunch& L, hipStream_t stream) {
+hipError_t launch_read_t(const ReadLaunch& L, hipStream_t stream, float* slot_part = nullptr) {
   const ReadGeometry g = read_geometry(L.d_ff, L.d_model, L.state_bf16, L.n_owners);
   ReadParams p;
   p.x = L.x;
   p.y = L.y;
   p.w0 = L.w0;
-  p.part = static_cast<float*>(L.workspace);
+  p.part = slot_part ? slot_part : static_cast<float*>(L.workspace);
+  p.slot_part = slot_part ? 1 : 0;
   p.count = L.count;
   p.d_ff = L.d_ff;
   p.d_model = L.d_model;
@@ -921,6 +926,7 @@ hipError_t launch_write_t(const WriteLaunch& L, hipStream_t stream) {
       q.y = L.y;
       q.w0 = nullptr;
       q.part = p.tpart;
+      q.slot_part = 0;
       q.count = L.count;
       q.d_ff = L.d_ff;
       q.d_model = L.d_model;
@@ -1001,6 +1007,64 @@ hipError_t launch_read(const ReadLaunch& L, hipStream_t stream) {
   }
   return L.state_bf16 ? launch_read_t<float, uint16_t>(L, stream)
                       : launch_read_t<float, float>(L, stream);
+}
+
+// ---------------------------------------------------------------------------
+// READ for callers that cannot allocate device memory
+// ---------------------------------------------------------------------------
+//
+// The split-K partial sums go to a static device array instead of the
+// context's workspace, one region per group slot.  Every GPU the library runs
+// on holds its own copy of the array until the process ends.  Host code never
+// passes the array's name to a kernel (on the host it is only a stand-in): its
+// device address is looked up once per device, with that device current, and
+// kept.  Every block writes its whole partial tile before the reduce reads it,
+// so the array needs no clearing between calls; calls that overlap on one GPU
+// share it and race.
+
+static __device__ __align__(256) float scratch[RWTTT_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices] = {};   // the array's device address, per device
+
+// The device address of `scratch` on the current device, looked up on the
+// first call with that device current.
+static hipError_t scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+size_t read_noalloc_bytes(int d_ff, int d_model, int state_bf16, int count) {
+  const ReadGeometry g = read_geometry(d_ff, d_model, state_bf16, count);
+  return g.part_floats * sizeof(float);
+}
+
+hipError_t launch_read_noalloc(const ReadLaunch& L, hipStream_t stream) {
+  if (read_noalloc_bytes(L.d_ff, L.d_model, L.state_bf16, L.count) > RWTTT_NOALLOC_SCRATCH_BYTES)
+    return hipErrorInvalidValue;
+  void* ptr = nullptr;
+  const hipError_t e = scratch_address(&ptr);
+  if (e != hipSuccess) return e;
+  float* part = static_cast<float*>(ptr);
+  if (L.io_bf16) {
+    return L.state_bf16 ? launch_read_t<uint16_t, uint16_t>(L, stream, part)
+                        : launch_read_t<uint16_t, float>(L, stream, part);
+  }
+  return L.state_bf16 ? launch_read_t<float, uint16_t>(L, stream, part)
+                      : launch_read_t<float, float>(L, stream, part);
 }
 
 hipError_t launch_tail_append(const TailLaunch& L, hipStream_t stream) {

@@ -30,7 +30,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 20
+    assert len(names) == 21
     out = subprocess.run(["nm", "-D", "--defined-only", R.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (rwttt_\w+)", out))
@@ -352,3 +352,31 @@ def test_plain_c_client_builds_against_the_header_and_runs(tmp_path):
     r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
     assert r.returncode == 0, r.stderr
     assert r.stdout.strip() == "ok"
+
+
+def test_noalloc_read_validates_before_touching_the_device():
+    """rwttt_read_noalloc refuses, on the host, what it cannot run: a group whose
+    partial sums exceed the static array (d_ff 14336, d_model 4096, fp32 state:
+    56 x 4096 fp32 values = 917,504 bytes per owner, so 18 owners fit in 16 MiB
+    and 19 do not), an adapter context, a stale planned version, an alias."""
+    assert R.RWTTT_NOALLOC_SCRATCH_BYTES == 16 << 20
+    assert 18 * 56 * 4096 * 4 <= R.RWTTT_NOALLOC_SCRATCH_BYTES < 19 * 56 * 4096 * 4
+    ctx, _ = host_ctx(n_owners=20, n_layers=1, d_ff=14336, d_model=4096, max_group=20)
+    g19 = R.make_group(R.RWTTT_READ, 0, 19)
+    assert R.rwttt_read_noalloc(ctx, g19, R.u32_array(range(19)), 0, 0x1000, 0x2000) == R.RWTTT_E_CAPACITY
+    g2 = R.make_group(R.RWTTT_READ, 0, 2)
+    assert R.rwttt_read_noalloc(ctx, g2, R.u32_array([3, 3]), 0, 0x1000, 0x2000) == R.RWTTT_E_OWNER_ALIAS
+    assert R.rwttt_read_noalloc(ctx, g2, R.u32_array([3, 4]), 0, 0x1000, 0x2000,
+                                expected=[0, 2]) == R.RWTTT_E_STALE_VERSION
+    assert R.rwttt_read_noalloc(ctx, g2, R.u32_array([3, 4]), 1, 0x1000, 0x2000) == R.RWTTT_E_INVALID
+    empty = R.make_group(R.RWTTT_READ, 0, 0)
+    assert R.rwttt_read_noalloc(ctx, empty, R.u32_array([]), 0, 0x1000, 0x2000) == R.RWTTT_OK
+    R.rwttt_destroy(ctx)
+    w0 = [0x10000]
+    slots = [0x1000000 + 0x1000 * i for i in range(4)]
+    cfg = R.make_config(2, 1, 64, 32, R.RWTTT_BF16, R.RWTTT_F32, 2, w0, slots,
+                        backend=R.RWTTT_DELTA_ADAPTER, rank=4)
+    actx = R.rwttt_create(cfg)
+    g1 = R.make_group(R.RWTTT_READ, 0, 1)
+    assert R.rwttt_read_noalloc(actx, g1, R.u32_array([0]), 0, 0x1000, 0x2000) == R.RWTTT_E_INVALID
+    R.rwttt_destroy(actx)
