@@ -13,10 +13,21 @@ B, and its dynamic-traffic study, Section 5.3).
 
 Trace kinds (one decode stream per request, fixed prefill):
   uniform        all streams ready at t = 0, update boundaries aligned;
-  phase_skew     all ready at t = 0, boundaries spread evenly over the chunk;
+  phase_skew     streams out of phase: stream s becomes decode-ready one
+                 full-batch decode step after stream s - 1 (its fixed prefill
+                 ends later), update boundaries counted from each stream's
+                 own decode start, so unless the start-up skew is absorbed by
+                 waiting the streams reach their boundaries on different steps;
   poisson        decode-ready times from a Poisson process, boundaries aligned
                  to each stream's own start;
   heterogeneous  ready at t = 0, decode lengths drawn from [n/4, 2n].
+
+Time model: every decode step takes time, issued or not.  A step that issues
+groups costs their measured service times (plus a fixed per-step overhead);
+a step in which every ready event is deferred by the wait budget still costs
+one idle tick, by default a full-batch decode step (a READ group of the target
+size B, or of every stream when B = 0, through every layer): the loop's
+cadence, so that waiting is paid for in latency.
 
 A request's i-th decode token (1-based, counted from its chunk phase) is a
 WRITE step when (phase + i) is a multiple of the chunk size C, else a READ.
@@ -58,6 +69,7 @@ class ServiceModel:
     write_us: dict
     step_overhead_us: float = 0.0
     source: str = ""
+    idle_step_us: float = None      # a step with nothing issued; None: a full-batch READ step
 
     @staticmethod
     def _at(table, b):
@@ -80,17 +92,25 @@ class ServiceModel:
         per_layer = self.read(b) if effect == READ else self.write(b, chunk)
         return self.layers * per_layer
 
+    def tick_us(self, batch):
+        """Time of a decode step in which every ready event waits: the fixed
+        idle step if set, else one READ step of ``batch`` owners."""
+        if self.idle_step_us is not None:
+            return float(self.idle_step_us)
+        return self.step_overhead_us + self.group_us(READ, batch, 0)
+
     def to_json(self, path):
         json.dump({"layers": self.layers, "read_us": self.read_us,
                    "write_us": {str(k): v for k, v in self.write_us.items()},
-                   "step_overhead_us": self.step_overhead_us, "source": self.source},
+                   "step_overhead_us": self.step_overhead_us, "source": self.source,
+                   "idle_step_us": self.idle_step_us},
                   open(path, "w"), indent=1)
 
     @classmethod
     def from_json(cls, path):
         d = json.load(open(path))
         return cls(d["layers"], d["read_us"], {int(k): v for k, v in d["write_us"].items()},
-                   d.get("step_overhead_us", 0.0), d.get("source", ""))
+                   d.get("step_overhead_us", 0.0), d.get("source", ""), d.get("idle_step_us"))
 
 
 # ---------------------------------------------------------------------------
@@ -105,14 +125,17 @@ class Request:
     phase: int              # tokens of the current chunk already seen at decode start
 
 
-def make_requests(kind, n_streams=8, n_tokens=512, chunk=128, seed=0, mean_gap_ms=50.0):
+def make_requests(kind, n_streams=8, n_tokens=512, chunk=128, seed=0, mean_gap_ms=50.0,
+                  step_s=0.0):
+    """``step_s``: one full-batch decode step in seconds, the phase-skew
+    trace's spacing of decode-ready times."""
     rng = np.random.default_rng(seed)
     reqs = []
     t = 0.0
     for s in range(n_streams):
         ready, n, phase = 0.0, n_tokens, 0
         if kind == "phase_skew":
-            phase = (s * chunk) // n_streams
+            ready = s * step_s
         elif kind == "poisson":
             if s:
                 t += float(rng.exponential(mean_gap_ms * 1e-3))
@@ -147,9 +170,15 @@ def _shape(effect, chunk):
     return (chunk << 1) | 1 if effect == WRITE else 0
 
 
+def decode_tick_us(model, B, n_streams):
+    """The idle-step tick of a run with target group size B over n streams."""
+    return model.tick_us(B if B > 0 else n_streams)
+
+
 def simulate(reqs, model, chunk=128, B=0, w=0, max_steps=1_000_000):
     """Replay requests through rwttt_plan with target group size B and wait budget w."""
     n = len(reqs)
+    tick = decode_tick_us(model, B, n)
     fake = [0x1000 * (i + 1) for i in range(2 * n + 1)]
     cfg = R.make_config(n, 1, 8, 8, R.RWTTT_BF16, R.RWTTT_F32, min(n, R.RWTTT_MAX_GROUP),
                         fake[:1], fake[1:])          # host-only context: planning only
@@ -181,7 +210,8 @@ def simulate(reqs, model, chunk=128, B=0, w=0, max_steps=1_000_000):
             if plan.status != R.RWTTT_OK:
                 raise R.RwtttError(plan.status, "rwttt_plan")
             issued = []
-            t_step = model.step_overhead_us if plan.n_groups else 0.0
+            # a step in which everything waits still takes one decode-step tick
+            t_step = model.step_overhead_us if plan.n_groups else tick
             for gi in range(plan.n_groups):
                 g = plan.group(gi)
                 owners = plan.owners(gi)
@@ -233,7 +263,9 @@ def sweep(model, kind="phase_skew", waits=(0, 1, 2, 4, 8, 16), seeds=range(5), n
     B = n_streams if B is None else B
     rows = []
     for w in waits:
-        res = [simulate(make_requests(kind, n_streams, n_tokens, chunk, seed), model, chunk, B, w)
+        step_s = 1e-6 * decode_tick_us(model, B, n_streams)
+        res = [simulate(make_requests(kind, n_streams, n_tokens, chunk, seed, step_s=step_s),
+                        model, chunk, B, w)
                for seed in seeds]
         rows.append(dict(w=w, tok_s=float(np.mean([r.tok_s for r in res])),
                          first_token_p95_ms=float(np.mean([r.first_token_p95_ms for r in res])),
