@@ -380,3 +380,52 @@ def test_noalloc_read_validates_before_touching_the_device():
     g1 = R.make_group(R.RWTTT_READ, 0, 1)
     assert R.rwttt_read_noalloc(actx, g1, R.u32_array([0]), 0, 0x1000, 0x2000) == R.RWTTT_E_INVALID
     R.rwttt_destroy(actx)
+
+
+class _Ev:
+    """Stand-in for a pair of HIP events: elapsed_time(end) gives the span in ms."""
+
+    def __init__(self, ms):
+        self.ms = ms
+
+    def elapsed_time(self, end):
+        return end.ms - self.ms
+
+
+def test_bench_counts_algorithmic_bytes_and_flops_per_call():
+    """The bench's per-call accounting: a READ of B owners moves W0 once, each
+    live state, x and y; a WRITE moves live, shadow, Z and G per owner and does
+    2 C d_ff d_model flops; a WRITE step's token adds x and y, and its second
+    W0 pass (plus the live state when not fused) is reported, not counted."""
+    sys.path.insert(0, ROOT)
+    import bench
+    from rwttt_inputs import workload
+    wl = workload(2)                          # bf16 io, fp32 state, 9728 x 2560
+    K, N, io, st = wl.d_ff, wl.d_model, 2, 4
+    t = bench.LaunchTimer(None)
+    t.records = [("read", 8, 0, _Ev(0.0), _Ev(1.0), 10), ("read", 7, 0, _Ev(1.0), _Ev(1.5), 4),
+                 ("write_token", 1, 64, _Ev(0.0), _Ev(0.5), 10)]
+    s = t.summary(wl)
+    rd = K * N * (io + 8 * st) + 8 * io * (K + N)
+    rd7 = K * N * (io + 7 * st) + 7 * io * (K + N)
+    assert s["read"]["bytes"] == 10 * rd + 4 * rd7
+    assert s["read"]["launches"] == 14 and s["read"]["total_ms"] == pytest.approx(1.5)
+    assert s["read"]["gbs"] == pytest.approx((10 * rd + 4 * rd7) / 1.5e-3 / 1e9)
+    w = s["write_token"]
+    assert w["bytes"] == 10 * (2 * st * K * N + io * 64 * (K + N) + io * (K + N))
+    assert w["bytes"] // 10 == 200826880                      # 200.8 MB per one-owner call
+    assert w["flops"] == 10 * 2.0 * 64 * K * N
+    assert w["token_extra_bytes"] == 10 * K * N * io          # W0 once per call, fused token
+    rec = bench.write_record(wl, s)
+    assert rec["hbm_frac"] == pytest.approx(w["bytes"] / 0.5e-3 / 1e9 / 8000.0, rel=1e-3)
+    assert rec["token_extra_bytes_per_launch"] == K * N * io
+    assert rec["kernel"].startswith("write_stream_kernel")
+    # C = 512 with a token: a READ of the group first (W0 and the live state again)
+    w4 = workload(4)
+    K4, N4 = w4.d_ff, w4.d_model
+    t.records = [("write_token", 8, 512, _Ev(0.0), _Ev(0.6), 1), ("write", 8, 512, _Ev(0.0), _Ev(0.6), 1)]
+    s4 = t.summary(w4)
+    assert s4["write_token"]["token_extra_bytes"] == K4 * N4 * 2 + 8 * 2 * K4 * N4
+    assert s4["write"]["token_extra_bytes"] == 0
+    assert s4["write"]["bytes"] == 8 * (2 * 2 * K4 * N4 + 2 * 512 * (K4 + N4))
+    assert bench.write_record(w4, {"write": s4["write"]})["kernel"] == "write_gemm_kernel"
