@@ -583,3 +583,53 @@ def test_write_bf16_state_rounding_is_exact(chunk):
                    O.bf16_round(O.widen(L, "bf16") + O.widen(G[chunk - 1], "bf16")[None, :]))
     say("inexact sums (rounded):", ties)
     assert np.array_equal(got, want)
+
+
+# --------------------------------------------------------------------------
+# degenerate updates: eta = 0 or Z = 0 leave the candidate equal to live, bit for bit
+# --------------------------------------------------------------------------
+
+DEGENERATE_CASES = [
+    # d_ff, d_model, io, state, chunk: the streaming kernel, the GEMM, the fp32-evidence kernel
+    (1000, 264, "bf16", "f32", 17),
+    (1000, 264, "bf16", "bf16", 64),
+    (520, 264, "bf16", "bf16", 150),
+    (520, 264, "bf16", "f32", 100),
+    (256, 64, "f32", "f32", 4),
+    (264, 520, "f32", "bf16", 5),
+]
+
+
+@pytest.mark.parametrize("d_ff,d_model,io,state,chunk", DEGENERATE_CASES)
+def test_zero_step_or_zero_evidence_gives_a_candidate_equal_to_live(d_ff, d_model, io, state, chunk):
+    """With eta = 0 (and random evidence), or with Z = 0 (and eta = 1), the
+    candidate dW + eta Z^T G is exactly the live state (Section 3, Write with
+    a null update), in both state dtypes and on every WRITE kernel; the token is
+    still the READ at version v."""
+    wl = small_workload(d_ff, d_model, io, state, 3)
+    say("degenerate write", d_ff, d_model, io, state, chunk)
+    src = TensorSource(wl)
+    sess = Session(wl, src)
+    Z = to_device(draw((chunk, d_ff), 1.0, io, wl.seed, (96, 1), absval=True), io)
+    G = to_device(draw((chunk, d_model), 1.0, io, wl.seed, (97, 1)), io)
+    Z0 = torch.zeros_like(Z)
+    live = slot_hash(sess.live(1, 0))
+    for zz, eta in ((Z, 0.0), (Z0, 1.0)):
+        assert write_group(sess, [1], 0, chunk, [zz], [G], eta=eta) == R.RWTTT_OK
+        torch.cuda.synchronize()
+        assert slot_hash(sess.shadow(1, 0)) == live, eta
+        assert R.rwttt_commit(sess.ctx, [1]) == R.RWTTT_OK
+        torch.cuda.synchronize()
+        assert slot_hash(sess.live(1, 0)) == live
+    assert sess.version(1) == (2, False)
+    # with a token the step's output is the READ of the unchanged state
+    X = draw((3, d_ff), 1.0, io, wl.seed, (98,))
+    xd = to_device(X, io)
+    tdt = torch.float32 if io == "f32" else torch.bfloat16
+    y = torch.zeros((3, d_model), dtype=tdt, device="cuda")
+    assert write_group(sess, [1], 0, chunk, [Z0], [G], eta=1.0, x_dev=xd, y_dev=y) == R.RWTTT_OK
+    torch.cuda.synchronize()
+    ref = O.round_to(O.read_apply(O.widen(X[1], io), O.widen(src.w0(0), io),
+                                  O.widen(src.dw_init(1, 0), state)), io)
+    assert O.max_rel_floor(host_f64(y[1], io), ref) <= out_tol(io)
+    assert slot_hash(sess.shadow(1, 0)) == live
