@@ -30,7 +30,11 @@ namespace {
 //    W0 term is fused into the same pass.  The W0 tile is the same for every
 //    slot: the blocks of all slots for one (chunk, tile) are placed on one XCD
 //    (dispatch is round-robin over the 8 XCDs by block index) so that W0 comes
-//    from HBM once and is re-read from that XCD's L2.  dW is streamed with
+//    from HBM once and is re-read from that XCD's L2.  Which XCD takes a pair
+//    rotates with the pair's round of eight: with 10 column tiles a fixed
+//    pair % 8 gave the even XCDs only even tiles, whose blocks ran ~7% slower
+//    than the odd tiles' (3% once every XCD mixes both: an address effect,
+//    not an XCD one), so those XCDs finished last.  dW is streamed with
 //    non-temporal loads so it does not evict W0.  The four waves' sums are
 //    added through LDS in a fixed order into one partial per (owner, chunk).
 // 2. read_reduce_kernel: y[b, n] = sum over chunks: four contiguous quarters
@@ -68,12 +72,14 @@ __global__ void __launch_bounds__(kReadThreads) read_partial_kernel(const ReadPa
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  // block -> (XCD, position on that XCD) -> ((chunk, tile) pair, slot)
+  // block -> (XCD, position on that XCD) -> ((chunk, tile) pair, slot).  Round
+  // pl of eight pairs is dealt to the XCDs rotated by pl, so that each XCD
+  // gets column tiles of both parities even when the tile count is even
   const int xcd = blockIdx.x & 7;
   const int pos = blockIdx.x >> 3;
   const int pl = pos / p.count;
   const int b = pos - pl * p.count;
-  const int pair = pl * 8 + xcd;
+  const int pair = pl * 8 + ((xcd + pl) & 7);
   if (pair >= p.ks * p.nt) return;
   const int kc = pair / p.nt;
   const int nt = pair - kc * p.nt;
