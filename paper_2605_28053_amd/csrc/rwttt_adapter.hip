@@ -63,14 +63,17 @@ __device__ __forceinline__ void lds_barrier() {
 // 1. adapter_read_partial_kernel: one 512-thread block per (K chunk of 192
 //    rows, column tile, group of up to 8 owners); each lane streams 16 bytes
 //    of every W0 row of the tile once and applies it to all the block's
-//    owners.  The eight waves split the chunk's rows, 24 each, and request all
-//    of them before any arithmetic (after the x chunk, so that staging x does
-//    not wait for W0).  Each owner's wave sums are added in wave order into
-//    one partial per (owner, chunk, tile).  Owner groups of one (chunk, tile)
-//    sit on one XCD (dispatch is round-robin over the 8 XCDs).  The chunk's
-//    tile blocks also form the owners' chunk shares of u = x A (r values
-//    each, ordered two-level sums), owner g in tile g mod (tiles), and the
-//    first tile's block appends the x chunk to the owners' tails if asked.
+//    owners.  The eight waves split the chunk's rows, 24 each.  A wave requests
+//    the x values of its own rows (every owner of the group), then the u
+//    share's x and A values, then all of its W0 rows, and only then waits:
+//    loads of one wave return in order, so x arrives first, and no wave waits
+//    for another's x before requesting W0.  Each owner's wave sums are added
+//    in wave order into one partial per (owner, chunk, tile).  Owner groups of
+//    one (chunk, tile) sit on one XCD (dispatch is round-robin over the 8
+//    XCDs).  The chunk's tile blocks also form the owners' chunk shares of
+//    u = x A (r values each, ordered two-level sums), owner g in tile
+//    g mod (tiles), and the first tile's block appends the x chunk to the
+//    owners' tails if asked.
 // 2. adapter_read_reduce_kernel: u = sum of the chunks' shares in chunk
 //    order; y[n] = (sum of the W0 partials: four contiguous quarters of the
 //    chunks, each in chunk order, then the quarters in order) +
@@ -118,32 +121,37 @@ adapter_read_partial_kernel(const AReadParams p) {
   const int b0 = gi * kAGroup;
   const int ng = min(kAGroup, p.count - b0);
 
-  // 1. requests, in the order they are needed: the x chunk and the first eight
-  //    A columns of the rows this lane takes in the u share; once x is staged,
-  //    this wave's W0 rows.  Every request is unconditional (indices clamped into
-  //    the buffers, unused values zeroed afterwards) so that no load waits
-  //    inside a branch.
+  // 1. requests, in the order they are needed, every one unconditional
+  //    (indices clamped into the buffers, unused values zeroed afterwards) so
+  //    that no load waits inside a branch.
   uint32_t rows[kAGroup];   // owner rows of the group's slots (block-uniform)
 #pragma unroll
   for (int g = 0; g < kAGroup; ++g) rows[g] = p.row[b0 + min(g, ng - 1)];
-  constexpr int XPER = kAGroup * kAChunk / kAThreads;
-  IO xv[XPER];   // raw until staged
+  // this wave's x values: its 24 rows of every owner of the group (lane l
+  // holds value l + 64 t: owner (l + 64 t) / 24, row (l + 64 t) % 24)
+  constexpr int XW = kAGroup * kARows / 64;
+  const int kw0 = wave * kARows;
+  IO xw[XW];
 #pragma unroll
-  for (int i = 0; i < XPER; ++i) {
-    const int idx = tid + i * kAThreads;
-    const int g = idx / kAChunk, k = idx - g * kAChunk;
+  for (int t = 0; t < XW; ++t) {
+    const int idx = lane + 64 * t;
+    const int g = idx / kARows, k = idx - g * kARows;
     uint32_t r = rows[0];
 #pragma unroll
     for (int g2 = 1; g2 < kAGroup; ++g2) r = g == g2 ? rows[g2] : r;
-    xv[i] = static_cast<const IO*>(p.x)[size_t(r) * p.d_ff + k0 + min(k, kn - 1)];
+    xw[t] = static_cast<const IO*>(p.x)[size_t(r) * p.d_ff + k0 + min(kw0 + k, kn - 1)];
   }
-  asm volatile("" ::: "memory");   // requests leave in this order
   // u share (step 2): wave i takes owner nt + i * tiles of the group; its lanes
-  // hold rows lane, lane + 64, lane + 128 of the chunk.  Their first eight A
-  // columns are requested here, by the waves that have an owner.
+  // hold rows lane, lane + 64, lane + 128 of the chunk: their x values and
+  // their first eight A columns
   const int ug = nt + wave * p.nt;
   const ST* uA = static_cast<const ST*>(p.state[b0 + (ug < ng ? ug : 0)]);
+  const uint32_t urow = p.row[b0 + (ug < ng ? ug : 0)];
+  IO xu[kAURows];
   float apre[kAURows][8];
+#pragma unroll
+  for (int r = 0; r < kAURows; ++r)
+    xu[r] = static_cast<const IO*>(p.x)[size_t(urow) * p.d_ff + k0 + min(lane + 64 * r, kn - 1)];
   if (ug < ng) {
 #pragma unroll
     for (int r = 0; r < kAURows; ++r) {
@@ -157,27 +165,24 @@ adapter_read_partial_kernel(const AReadParams p) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) apre[r][j] = 0.f;
   }
-  __builtin_amdgcn_sched_barrier(0);   // x is waited for only after the A requests are out
-  // the x chunk is staged before the W0 rows are requested: under the W0
-  // stream its few loads would come back last
-#pragma unroll
-  for (int i = 0; i < XPER; ++i) {
-    const int idx = tid + i * kAThreads;
-    const int g = idx / kAChunk, k = idx - g * kAChunk;
-    const bool ok = g < ng && k < kn;
-    xs[k][g] = ok ? to_f32(xv[i]) : 0.f;
-    if constexpr (sizeof(IO) == 2) xh[k >> 1][g][k & 1] = ok ? xv[i] : uint16_t(0);
-  }
-  lds_barrier();
-  // rows past the chunk repeat its last row (their x is zero); lanes past
-  // d_model read column 0 and their sums are dropped
-  const int kw0 = wave * kARows;
+  // then this wave's W0 rows; rows past the chunk repeat its last row (their
+  // x is zero); lanes past d_model read column 0 and their sums are dropped
   const IO* wbase = static_cast<const IO*>(p.w0) + size_t(k0) * p.d_model + (col_ok ? col : 0);
   Packed<IO, COLS> w[kARows];
 #pragma unroll
   for (int u = 0; u < kARows; ++u)
     load_packed<false>(wbase + size_t(min(kw0 + u, kn - 1)) * p.d_model, w[u]);
-  __builtin_amdgcn_sched_barrier(0);   // every W0 request is out before any arithmetic
+  __builtin_amdgcn_sched_barrier(0);   // every request is out before x is waited for
+  // the wave stages its own rows of x (no other wave reads them before the
+  // block barrier below; LDS requests of one wave complete in order)
+#pragma unroll
+  for (int t = 0; t < XW; ++t) {
+    const int idx = lane + 64 * t;
+    const int g = idx / kARows, k = kw0 + idx - (idx / kARows) * kARows;
+    const bool ok = g < ng && k < kn;
+    xs[k][g] = ok ? to_f32(xw[t]) : 0.f;
+    if constexpr (sizeof(IO) == 2) xh[k >> 1][g][k & 1] = ok ? xw[t] : uint16_t(0);
+  }
 
   // 2. u share of this chunk for the wave's owner: sum_k x[k] A[k][j], eight
   //    rank columns per pass: each lane sums its rows in order, then a
@@ -192,7 +197,7 @@ adapter_read_partial_kernel(const AReadParams p) {
 #pragma unroll
     for (int r = 0; r < kAURows; ++r) {
       const int k = lane + 64 * r;
-      const float xk = xs[k][ug];   // zero past the chunk
+      const float xk = k < kn ? to_f32(xu[r]) : 0.f;   // zero past the chunk
       const size_t at = size_t(k0 + min(k, kn - 1)) * p.rank;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
