@@ -450,7 +450,7 @@ constexpr int kGStage = kGStageA + kGKC * kGTN;           // 24 KB per stage
 constexpr int kGUnitsA = kGStageA * 2 / 1024;             // 1 KB copies of Z per stage (16)
 constexpr int kGUnits = kGStage * 2 / 1024;               // 1 KB copies per stage (24)
 constexpr int kGCopies = kGUnits / 4;                     // copies per wave per stage (6)
-constexpr int kGColGroups = 4;                            // column-tile groups over the XCDs
+constexpr int kGColGroups = 2;                            // column-tile groups over the XCDs
 constexpr int kGRowClasses = 8 / kGColGroups;             // row-tile classes over the XCDs
 
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
@@ -487,7 +487,10 @@ __device__ __forceinline__ i32x4_t gemm_rsrc(const void* p, int bytes) {
 // One 1 KB stage copy: lane l's 16 bytes at byte offset voff of the buffer go
 // to LDS at dst + 16 l.  Issued as inline assembly so that the compiler does
 // not add its own (conservative) waits for LDS copies: every read of a stage
-// is preceded by an explicit vmcnt wait and a barrier.
+// is preceded by an explicit vmcnt wait and a barrier.  NT marks the data as
+// streamed once (the live state), so that it does not displace the operand
+// tiles that the XCD's other blocks still read from L2.
+template <bool NT = false>
 __device__ __forceinline__ void gemm_copy(uint16_t* dst, uint32_t voff, i32x4_t rsrc) {
   const uint32_t lds = uint32_t(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint16_t*)dst));
   // the descriptor and the LDS address are wave-uniform: keep them in SGPRs
@@ -495,8 +498,12 @@ __device__ __forceinline__ void gemm_copy(uint16_t* dst, uint32_t voff, i32x4_t 
                      __builtin_amdgcn_readfirstlane(rsrc[2]), __builtin_amdgcn_readfirstlane(rsrc[3])};
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-               :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(r) : "memory", "m0");
+  if constexpr (NT)
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen nt lds"
+                 :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(r) : "memory", "m0");
+  else
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :: "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(r) : "memory", "m0");
 #pragma clang diagnostic pop
 }
 
@@ -521,9 +528,11 @@ write_gemm_kernel(const WriteParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
   // block -> (owner, row tile, column tile).  Blocks are dealt to the 8
-  // XCDs round-robin; XCD x takes column-tile group x % 4 and the row tiles
-  // of parity x / 4, so each G column tile is read by two XCDs and each Z row
-  // tile by four, and consecutive blocks of an XCD share their Z row tile.
+  // XCDs round-robin; XCD x takes column-tile half x % 2 and the row tiles
+  // congruent to x / 2 mod 4, so each Z row tile is read by two XCDs and each
+  // G column tile by four.  Consecutive blocks of an XCD share their Z row
+  // tile, and the XCD's G columns (2 MB at C = 512) stay in its L2 while the
+  // live state streams past them non-temporally.
   const int xcd = blockIdx.x & 7;
   const int pos = blockIdx.x >> 3;
   const int ntg = (p.ntl + kGColGroups - 1) / kGColGroups;
@@ -624,7 +633,7 @@ write_gemm_kernel(const WriteParams p) {
       const int r = 4 * t + (lane >> 4);
       const int col = n0 + 8 * ((lane & 15) ^ (r & 15));
       const uint32_t off = col < p.d_model ? uint32_t(r * p.d_model + col) * 2u : 0x80000000u;
-      gemm_copy(dst + t * 512, off, lr);
+      gemm_copy<true>(dst + t * 512, off, lr);
     }
   };
 
