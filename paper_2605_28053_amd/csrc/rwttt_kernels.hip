@@ -231,14 +231,17 @@ int stream_parts(int d_ff, int d_model) {
   return (mt + items - 1) / items;
 }
 
-template <typename T>
+// Rows m0 + 8 wave .. + 7 of a [d_ff, d_model] matrix, 4 columns at ncol.  The
+// live state is read once (non-temporal); W0 is read by every slot of the
+// group from the same XCD and must stay in its L2 (NT = false).
+template <bool NT = true, typename T>
 __device__ __forceinline__ void stream_load_rows(const T* base, int d_ff, int d_model, int m0,
                                                  int wave, int ncol, bool ncol_ok,
                                                  Packed<T, 4> (&v)[kSTM / 4]) {
 #pragma unroll
   for (int rr = 0; rr < kSTM / 4; ++rr) {
     const int m = m0 + wave * (kSTM / 4) + rr;
-    if (m < d_ff && ncol_ok) load_packed<true>(base + size_t(m) * d_model + ncol, v[rr]);
+    if (m < d_ff && ncol_ok) load_packed<NT>(base + size_t(m) * d_model + ncol, v[rr]);
     else v[rr].zero();
   }
 }
@@ -321,7 +324,7 @@ write_stream_kernel(const WriteParams p) {
   stream_load_rows(live, p.d_ff, p.d_model, part * kSTM, wave, ncol, ncol_ok, lv);
   stream_load_pair(Z, p.d_ff, p.d_ff, p.chunk, part * kSTM, tid, za, zb);
   if (TOKEN) {
-    stream_load_rows(W0, p.d_ff, p.d_model, part * kSTM, wave, ncol, ncol_ok, wv);
+    stream_load_rows<false>(W0, p.d_ff, p.d_model, part * kSTM, wave, ncol, ncol_ok, wv);
     if (part * kSTM + wave * RPW < p.d_ff)
       xq = *reinterpret_cast<const uint4*>(X + part * kSTM + wave * RPW);
   }
@@ -341,7 +344,7 @@ write_stream_kernel(const WriteParams p) {
       stream_load_rows(live, p.d_ff, p.d_model, mn * kSTM, wave, ncol, ncol_ok, nx);
       stream_load_pair(Z, p.d_ff, p.d_ff, p.chunk, mn * kSTM, tid, za, zb);
       if (TOKEN) {
-        stream_load_rows(W0, p.d_ff, p.d_model, mn * kSTM, wave, ncol, ncol_ok, nw);
+        stream_load_rows<false>(W0, p.d_ff, p.d_model, mn * kSTM, wave, ncol, ncol_ok, nw);
         if (mn * kSTM + wave * RPW < p.d_ff)
           nxq = *reinterpret_cast<const uint4*>(X + mn * kSTM + wave * RPW);
       }
