@@ -440,8 +440,8 @@ write_stream_kernel(const WriteParams p) {
 //
 // The MFMA is issued as D^T = G^T Z, so the accumulators of a lane hold runs
 // of four consecutive columns of one state row.  The epilogue combines them
-// with the live rows in that layout (bf16 state: live copied into the freed
-// stages; fp32 state: a register epilogue through a private LDS region) and
+// with the live rows in that layout (bf16 state: live copied non-temporally
+// into the freed stages; fp32 state: a register epilogue through a private LDS region) and
 // stores whole rows, rounding to bf16 with the hardware packed convert.
 
 constexpr int kGTM = 256;                                 // rows (d_ff) per tile
