@@ -411,7 +411,7 @@ def run_cpu_baseline(args, wl, kept):
                        f"{dt:.2f} s measured, scaled x{wl.n_layers / len(layers):g} to all layers"))
     out["host"] = host_info()
     if threadpool_limits is not None:
-        steps1 = range(min(len(steps), 10))
+        steps1 = range(min(len(steps), 30))
         with threadpool_limits(limits=1):
             v1, dt1 = timed(steps1, layers[:1])
         out["single_thread"] = dict(value=v1, unit="tok/s", cores=1,
@@ -531,7 +531,7 @@ def main():
     ap.add_argument("--threads", type=int, default=16, help="host threads for input generation")
     ap.add_argument("--cpu-baseline", choices=["on", "off"], default=None,
                     help="time the oracle on a sample of the workload (default: on for workload 2)")
-    ap.add_argument("--cpu-steps", type=int, default=30)
+    ap.add_argument("--cpu-steps", type=int, default=100)
     ap.add_argument("--cpu-layers", type=int, nargs="+", default=[0, 1])
     ap.add_argument("--kernel-events", choices=["on", "off"], default="on")
     ap.add_argument("--streams", type=int, choices=[1, 2], default=1,
